@@ -1,0 +1,79 @@
+"""The oracle's pins must catch plausible mistakes in the oracle itself.
+
+Each case copies ``oracle/fwht_oracle.c``, plants one mistake (a flipped
+butterfly sign, a dropped stage, a wrong pair index, an off-by-one exponent
+bias, a missing scale, an ignored stride ...), compiles the copy on the CPU
+into a temporary library and runs the pin battery of ``test_oracle.py``
+against it.  At least one pin must fail for every mutant.  The real oracle
+source is never modified.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle as oracle_pkg
+import test_oracle as T
+
+MUTANTS = [
+    ("butterfly_sign", "v[j + h] = a - b;", "v[j + h] = b - a;"),
+    ("butterfly_sum_dropped_term", "v[j] = a + b;", "v[j] = a;"),
+    ("first_stage_dropped", "for (int64_t h = 1; h < n; h *= 2)", "for (int64_t h = 2; h < n; h *= 2)"),
+    ("last_stage_dropped", "for (int64_t h = 1; h < n; h *= 2)", "for (int64_t h = 1; 2 * h < n; h *= 2)"),
+    ("block_step_wrong", "for (int64_t i = 0; i < n; i += 2 * h)", "for (int64_t i = 0; i + h < n; i += h)"),
+    ("partner_index_wrong", "double b = v[j + h];", "double b = v[(j + h) ^ 1];"),
+    ("fp16_exponent_bias", "expo - 25", "expo - 24"),
+    ("fp16_subnormal_scale", "ldexp((double)frac, -24)", "ldexp((double)frac, -23)"),
+    ("fp16_implicit_bit", "(1024 + frac)", "(frac)"),
+    ("bf16_exponent_bias", "expo - 134", "expo - 133"),
+    ("bf16_fraction_width", "(128 + frac)", "(256 + frac)"),
+    ("scale_missing", "row[k] *= jb->scale;", "row[k] *= 1.0;"),
+    ("stride_ignored", "const uint16_t *src = jb->in + i * jb->in_stride;",
+     "const uint16_t *src = jb->in + i * jb->n;"),
+    ("direct_sign_parity", "(uint64_t)(cols[t] & k)", "(uint64_t)(cols[t] | k)"),
+    ("direct_scale_missing", "out[t] = acc * scale;", "out[t] = acc;"),
+    ("thread_remainder_rows_dropped", "jobs[t].row1 = m * (t + 1) / nthreads;",
+     "jobs[t].row1 = m * t / nthreads + m / nthreads;"),
+]
+
+
+def _pins(o):
+    """Callables that raise on failure; each is one pin of test_oracle.py."""
+    return [
+        lambda: T.test_decode_fp16_every_pattern(o),
+        lambda: T.test_decode_bf16_every_pattern(o),
+        lambda: T.test_matches_explicit_matrix_integers_exact(o, 4),
+        lambda: T.test_matches_explicit_matrix_integers_exact(o, 9),
+        lambda: T.test_matches_explicit_matrix_random(o, "bf16", 8),
+        lambda: T.test_matches_explicit_matrix_random(o, "fp16", 7),
+        lambda: T.test_matches_kronecker_factorisation(o, 8, 7),
+        lambda: T.test_direct_definition_agrees_with_explicit_matrix(o),
+        lambda: T.test_orthogonality_from_basis_vectors(o, 4),
+        lambda: T.test_hand_derived_fixtures(o),
+        lambda: T.test_strided_rows_ignore_gaps(o),
+        lambda: T.test_scale_is_one_final_product(o),
+        lambda: T.test_threads_do_not_change_results(o),
+    ]
+
+
+def test_pins_pass_on_the_real_oracle(oracle):
+    for pin in _pins(oracle):
+        pin()
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, name, old, new):
+    src = oracle_pkg.SOURCE.read_text()
+    assert old in src, f"mutation site for {name} not found in the oracle source"
+    mutated = tmp_path / "fwht_oracle_mutant.c"
+    mutated.write_text(src.replace(old, new, 1))
+    lib = oracle_pkg.compile_library(mutated, tmp_path / "liboracle_mutant.so")
+    o = oracle_pkg.Oracle(lib)
+    failures = []
+    with np.errstate(all="ignore"):
+        for i, pin in enumerate(_pins(o)):
+            try:
+                pin()
+            except (AssertionError, ValueError):
+                failures.append(i)
+    assert failures, f"mutant {name} passed every pin"
