@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Throughput of libhadacore's batched Walsh-Hadamard transform on one MI355X.
+
+One step = one call of the transform over one batch of synthetic input that is
+already resident in HBM.  Steps cycle through a rotating set of buffers of at
+least 1 GiB so that no call finds its data in the 256 MiB Infinity Cache.
+
+Default workload: bf16, m = 8 x 32 x 4096 = 1,048,576 rows of n = 128 (the
+attention head_dim rotation), in place, scale fp32(1/sqrt(128)).
+
+Prints ONE JSON line.  ``--sweep FILE`` additionally times every named
+workload and the n = 2^7..2^15 sweep (both dtypes, both modes) and writes one
+JSON line per point to FILE.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import re
+import sys
+import time
+from pathlib import Path
+
+ROOT = Path(__file__).resolve().parent
+if str(ROOT) not in sys.path:
+    sys.path.insert(0, str(ROOT))
+
+METRIC = "FWHT elements/s and achieved HBM GB/s (% of peak) per n, fp16/bf16"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+ROTATING_BYTES = 1 << 30       # rotating buffer set per workload (>> 256 MiB MALL)
+SOURCE = ROOT / "paper_2412_08832_amd" / "csrc" / "hadacore.hip"
+PROFILES = ROOT / "profiles"
+
+
+def parse_args(argv=None):
+    p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="c2", help="c1, c2, c3, c4 or sweep:<dtype>:<log2 n>:<in|out>")
+    p.add_argument("--sweep", metavar="FILE", help="also time every workload, one JSON line each")
+    p.add_argument("--cpu-seconds", type=float, default=10.0,
+                   help="target duration of the CPU oracle baseline sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args(argv)
+
+
+def workload_by_name(name: str):
+    from paper_2412_08832_amd import workloads as W
+    if name in W.CONFIGS:
+        return W.CONFIGS[name]
+    m = re.fullmatch(r"sweep:(fp16|bf16):(\d+):(in|out)", name)
+    if not m:
+        raise SystemExit(f"unknown workload {name!r}")
+    return W.sweep_point(int(m.group(2)), m.group(1), m.group(3) == "in")
+
+
+def source_digest() -> str:
+    return hashlib.sha256(SOURCE.read_bytes()).hexdigest()
+
+
+def measured_traffic(workload: str, digest: str):
+    """HBM bytes per launch from a committed rocprofv3 PMC summary, or None.
+
+    A summary counts only while the kernel source it was taken on is unchanged.
+    """
+    for path in sorted(PROFILES.glob("*.txt")):
+        text = path.read_text()
+        fields = dict(re.findall(r"^([a-z_0-9]+):\s*(\S+)\s*$", text, flags=re.M))
+        if fields.get("workload") == workload and fields.get("source_sha256") == digest:
+            try:
+                return int(float(fields["traffic_bytes_per_launch"]))
+            except (KeyError, ValueError):
+                return None
+    return None
+
+
+class Device:
+    def __init__(self):
+        import torch
+        from paper_2412_08832_amd import hadacore
+        if not torch.cuda.is_available():
+            raise SystemExit("bench.py needs a ROCm GPU")
+        self.torch = torch
+        self.H = hadacore
+        hadacore.library()  # raises if the HIP library is missing: there is no fallback
+        self.dev = torch.device("cuda:0")
+        torch.cuda.set_device(self.dev)
+        self.stream = torch.cuda.current_stream(self.dev)
+
+    def upload(self, bits, dtype: str):
+        import numpy as np
+        torch = self.torch
+        t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(self.dev)
+        return t.view(torch.float16 if dtype == "fp16" else torch.bfloat16)
+
+    def time_calls(self, calls, steps: int, warmup: int) -> float:
+        """Seconds for `steps` back-to-back calls (cycling through `calls`), HIP events
+        recorded on the stream the kernels are launched on."""
+        torch = self.torch
+        for i in range(warmup):
+            calls[i % len(calls)]()
+        torch.cuda.synchronize(self.dev)
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        start.record(self.stream)
+        for i in range(steps):
+            calls[i % len(calls)]()
+        end.record(self.stream)
+        end.synchronize()
+        torch.cuda.synchronize(self.dev)
+        return start.elapsed_time(end) / 1e3
+
+
+def time_workload(d: Device, w, steps: int, warmup: int) -> dict:
+    from paper_2412_08832_amd import workloads as W
+    H, torch = d.H, d.torch
+    bits = W.generate(w)
+    code = H.FP16 if w.dtype == "fp16" else H.BF16
+    nbytes = w.m * w.n * 2
+    per_set = nbytes if w.inplace else 2 * nbytes
+    nbuf = max(2, math.ceil(ROTATING_BYTES / per_set))
+    first = d.upload(bits, w.dtype)
+    del bits
+    ins = [first] + [first.clone() for _ in range(nbuf - 1)]
+    outs = ins if w.inplace else [torch.empty_like(first) for _ in range(nbuf)]
+    s = d.stream.cuda_stream
+    calls = [
+        (lambda i=i: H.hadamard_transform(ins[i].data_ptr(), outs[i].data_ptr(), w.m, w.n, code,
+                                          w.scale, s))
+        for i in range(nbuf)
+    ]
+    sec = d.time_calls(calls, steps, warmup)
+    per_launch = sec / steps
+    alg_bytes = 2 * nbytes                      # one read + one write of every element
+    gbs = alg_bytes / per_launch / 1e9
+
+    # device copy of the same bytes: the achievable-bandwidth reference
+    srcs = ins
+    dsts = [torch.empty_like(first) for _ in range(nbuf)] if w.inplace else outs
+    copies = [
+        (lambda i=i: H.hadacore_stream_copy(srcs[i].data_ptr(), dsts[i].data_ptr(), nbytes, s))
+        for i in range(nbuf)
+    ]
+    csec = d.time_calls(copies, steps, warmup) / steps
+    copy_gbs = alg_bytes / csec / 1e9
+    del ins, outs, srcs, dsts, first
+    torch.cuda.empty_cache()
+    return {
+        "workload": w.name, "dtype": w.dtype, "m": w.m, "n": w.n, "inplace": w.inplace,
+        "steps": steps, "rotating_buffers": nbuf, "ms_per_step": per_launch * 1e3,
+        "elements_per_s": w.m * w.n / per_launch, "gbs": gbs, "frac_hbm_peak": gbs / HBM_PEAK_GBS,
+        "copy_gbs": copy_gbs, "frac_of_copy": gbs / copy_gbs, "alg_bytes_per_launch": alg_bytes,
+    }
+
+
+def cpu_baseline(w, target_seconds: float) -> dict:
+    """The fp64 oracle on the host cores, timed on a bounded row sample of the workload."""
+    import numpy as np
+    import oracle
+    from paper_2412_08832_amd import workloads as W
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    cores = max(1, min(cores, 16))
+    orc = oracle.get()
+    probe_rows = max(1, min(w.m, (1 << 20) // w.n))
+    bits = W.generate(w, rows=probe_rows)
+    t0 = time.perf_counter()
+    orc.fwht(bits, w.dtype, w.scale, nthreads=cores)
+    rate = probe_rows * w.n / max(time.perf_counter() - t0, 1e-6)
+    rows = int(min(w.m, max(probe_rows, target_seconds * rate / w.n)))
+    bits = W.generate(w, rows=rows) if rows != probe_rows else bits
+    t0 = time.perf_counter()
+    orc.fwht(bits, w.dtype, w.scale, nthreads=cores)
+    sec = time.perf_counter() - t0
+    cpu = ""
+    try:
+        for line in Path("/proc/cpuinfo").read_text().splitlines():
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {
+        "value": rows * w.n / sec, "unit": "elements/s", "cores": cores, "kind": "oracle",
+        "sample": f"first {rows} of {w.m} rows ({rows * w.n} elements), {sec:.1f} s, "
+                  f"fp64 iterative FWHT in C on {cores} threads, {cpu}",
+    }
+
+
+def main(argv=None) -> int:
+    args = parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); rows are "
+              "independent, so N GPUs would each run this kernel on m/N rows.", file=sys.stderr)
+        return 2
+    w = workload_by_name(args.workload)
+    d = Device()
+    r = time_workload(d, w, args.steps, args.warmup)
+    digest = source_digest()
+    traffic = measured_traffic(w.name, digest)
+    line = {
+        "metric": METRIC,
+        "value": r["elements_per_s"],
+        "unit": "elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": r["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "m": w.m, "n": w.n, "io_dtype": w.dtype, "inplace": w.inplace,
+            "scale": w.scale, "rotating_buffers": r["rotating_buffers"],
+            "achieved_gbs": r["gbs"], "frac_hbm_peak": r["frac_hbm_peak"],
+            "copy_gbs": r["copy_gbs"], "frac_of_copy": r["frac_of_copy"],
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": r["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": r["frac_hbm_peak"], "traffic": traffic,
+        },
+    }
+    if args.sweep:
+        from paper_2412_08832_amd import workloads as W
+        points = [W.CONFIGS[k] for k in ("c1", "c2", "c3", "c4")]
+        for inplace in (True, False):
+            for dt in ("fp16", "bf16"):
+                points += [W.sweep_point(k, dt, inplace) for k in range(7, 16)]
+        with open(args.sweep, "w") as f:
+            for p in points:
+                pr = time_workload(d, p, args.steps, args.warmup)
+                f.write(json.dumps(pr) + "\n")
+                f.flush()
+                print(f"[sweep] {p.name}: {pr['gbs']:.0f} GB/s ({100 * pr['frac_hbm_peak']:.1f}% "
+                      f"of peak, {100 * pr['frac_of_copy']:.1f}% of copy)", file=sys.stderr,
+                      flush=True)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,111 @@
+/*
+ * hadacore.h -- C ABI of libhadacore: batched, normalized Walsh-Hadamard
+ * transform of fp16/bf16 rows on AMD Instinct MI355X (gfx950).
+ *
+ * Operation (HadaCore, arXiv 2412.08832, Sec. 2.1-2.2 and Sec. 2.4):
+ * for every row i < m of an m x n matrix x of 16-bit floats,
+ *
+ *     out[i][j] = scale * sum_{k<n} (-1)^popcount(j & k) * in[i][k],  j < n,
+ *
+ * i.e. each row is multiplied on the right by the Sylvester-ordered
+ * Walsh-Hadamard matrix H_n (natural order, +-1 entries), and by `scale`.
+ * The normalized transform of the paper is scale = 1/sqrt(n); H_n is never
+ * stored.  n is a power of two from 2^7 to 2^15 (Sec. 2.3-2.4 and Sec. 3.2
+ * bound the sizes at 2^15).  In-place operation (Appendix B) is supported.
+ *
+ * Numerics: inputs are widened exactly to fp32, multiplied by `scale` once
+ * (before the butterflies, so that large bf16 rows cannot overflow fp32
+ * partial sums), transformed with fp32 intermediates only, and rounded once
+ * to the output dtype with round-to-nearest-even.  Subnormals are preserved.
+ * NaN/Inf propagate as IEEE arithmetic dictates.  Results are deterministic:
+ * repeated calls, and in-place vs out-of-place calls, give identical bits.
+ *
+ * Memory: all pointers are DEVICE pointers owned by the caller; the library
+ * never allocates, frees or retains them.  Rows are contiguous (element
+ * stride 1) and start every `row_stride` elements; elements between n and the
+ * row stride are neither read nor written.
+ *
+ * Streams: work is enqueued asynchronously on `stream` (a hipStream_t; NULL
+ * means the default stream) and the call returns without synchronizing.
+ * Buffers must stay alive until that work completes.  Faults in the enqueued
+ * kernel surface at the caller's next synchronization, not here.
+ *
+ * Errors: arguments are validated synchronously before anything is enqueued;
+ * on error nothing is enqueued and a nonzero status is returned.  No call
+ * aborts or throws.  The library keeps no state beyond a per-device cache of
+ * the architecture check and is safe to call from several host threads.
+ */
+#ifndef HADACORE_H
+#define HADACORE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HADACORE_VERSION 10000 /* 1.0.0 */
+
+typedef int32_t hadacore_dtype;
+#define HADACORE_FP16 0 /* IEEE binary16 */
+#define HADACORE_BF16 1 /* bfloat16 */
+
+typedef int32_t hadacore_status;
+#define HADACORE_SUCCESS 0
+#define HADACORE_ERROR_INVALID_VALUE 1      /* m < 0, null pointer with m > 0, non-finite scale */
+#define HADACORE_ERROR_INVALID_SIZE 2       /* n not a power of two in [128, 32768] */
+#define HADACORE_ERROR_INVALID_DTYPE 3      /* dtype not HADACORE_FP16 / HADACORE_BF16 */
+#define HADACORE_ERROR_INVALID_STRIDE 4     /* row stride < n, or not a multiple of 8 elements */
+#define HADACORE_ERROR_MISALIGNED 5         /* in or out not 16-byte aligned */
+#define HADACORE_ERROR_OVERLAP 6            /* in/out overlap without being the same layout */
+#define HADACORE_ERROR_LAUNCH 7             /* the HIP runtime rejected the kernel launch */
+#define HADACORE_ERROR_UNSUPPORTED_DEVICE 8 /* current device is not gfx950 */
+#define HADACORE_ERROR_TOO_LARGE 9          /* m too large for one launch (m >= 2^31) */
+
+/*
+ * hadamard_transform -- out = scale * in * H_n for m dense rows of n elements.
+ *   in     device pointer to m*n 16-bit values, 16-byte aligned (read only
+ *          unless in == out)
+ *   out    device pointer to m*n 16-bit values, 16-byte aligned; out == in
+ *          selects in-place operation, any other overlap is rejected
+ *   m      number of rows, >= 0; m == 0 returns HADACORE_SUCCESS and enqueues
+ *          nothing (pointers may then be NULL)
+ *   n      transform length, a power of two in [128, 32768]
+ *   dtype  HADACORE_FP16 or HADACORE_BF16 (input and output share it)
+ *   scale  finite fp32 multiplier; 1/sqrt(n) gives the orthonormal transform
+ *   stream hipStream_t to enqueue on (NULL = default stream)
+ * Same as hadamard_transform_strided with both row strides equal to n.
+ */
+hadacore_status hadamard_transform(const void *in, void *out, int64_t m, int64_t n,
+                                   hadacore_dtype dtype, float scale, void *stream);
+
+/*
+ * hadamard_transform_strided -- as hadamard_transform, with row i of the input
+ * at in + i*in_row_stride and row i of the output at out + i*out_row_stride
+ * (strides in elements, each >= n and a multiple of 8).  In-place operation
+ * requires in == out and in_row_stride == out_row_stride.
+ */
+hadacore_status hadamard_transform_strided(const void *in, int64_t in_row_stride, void *out,
+                                           int64_t out_row_stride, int64_t m, int64_t n,
+                                           hadacore_dtype dtype, float scale, void *stream);
+
+/*
+ * hadacore_stream_copy -- copies `bytes` bytes from device pointer `src` to
+ * device pointer `dst` with 16-byte vector loads and stores on `stream`.  Both
+ * pointers 16-byte aligned, bytes a multiple of 16, ranges disjoint.  It moves
+ * the same HBM bytes per element as the transform and serves as its measured
+ * bandwidth ceiling (the paper's Appendix B compares against a device copy).
+ */
+hadacore_status hadacore_stream_copy(const void *src, void *dst, int64_t bytes, void *stream);
+
+/* Static, human-readable name of a status code (never NULL). */
+const char *hadacore_status_string(hadacore_status status);
+
+/* HADACORE_VERSION of the loaded library. */
+int32_t hadacore_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HADACORE_H */

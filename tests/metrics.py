@@ -74,45 +74,64 @@ class Comparison:
                 f"zero_row_mismatch={self.zero_row_mismatch}")
 
 
+class Accumulator:
+    """Accumulates the comparison over row blocks so that large matrices never
+    need all of their float64 temporaries at once."""
+
+    def __init__(self, dtype: str):
+        self.dtype = dtype
+        self.count = 0
+        self.num = 0.0
+        self.den = 0.0
+        self.max_floored = 0.0
+        self.max_unfloored = 0.0
+        self.above = 0
+        self.mismatch = 0
+        self.zero_mismatch = 0
+
+    def add(self, gpu: np.ndarray, ref: np.ndarray) -> "Accumulator":
+        gpu = np.asarray(gpu, dtype=np.float64)
+        ref = np.asarray(ref, dtype=np.float64)
+        if gpu.shape != ref.shape:
+            raise ValueError(f"shape mismatch {gpu.shape} vs {ref.shape}")
+        if ref.ndim == 1:
+            gpu = gpu[None, :]
+            ref = ref[None, :]
+        if ref.size == 0:
+            return self
+        fin = np.isfinite(ref)
+        gfin = np.isfinite(gpu)
+        self.mismatch += int(np.count_nonzero(np.isnan(ref) & ~np.isnan(gpu)))
+        self.mismatch += int(np.count_nonzero(np.isinf(ref) & (gpu != ref)))
+        self.mismatch += int(np.count_nonzero(fin & ~gfin))
+        both = fin & gfin
+        r = np.where(fin, ref, 0.0)
+        diff = np.where(both, gpu - r, 0.0)
+        self.den += float(np.sum(r * r))
+        self.num += float(np.sum(diff * diff))
+        rms = np.sqrt(np.mean(r * r, axis=1, keepdims=True))
+        absdiff = np.abs(diff)
+        floored = absdiff / ulp(np.maximum(np.abs(r), rms * 2.0 ** FLOOR_LOG2), self.dtype)
+        unfloored = absdiff / ulp(np.abs(r), self.dtype)
+        self.max_floored = max(self.max_floored, float(floored.max()))
+        self.max_unfloored = max(self.max_unfloored, float(unfloored.max()))
+        self.above += int(np.count_nonzero(unfloored > MAX_ULP_LIMIT))
+        zero_rows = np.all(r == 0, axis=1) & np.all(fin, axis=1)
+        if zero_rows.any():
+            g = np.where(gfin, gpu, 1.0)
+            self.zero_mismatch += int(np.count_nonzero(np.any(g[zero_rows] != 0, axis=1)))
+        self.count += int(ref.size)
+        return self
+
+    def result(self) -> Comparison:
+        if self.den > 0:
+            rel = float(np.sqrt(self.num / self.den))
+        else:
+            rel = 0.0 if self.num == 0 else float("inf")
+        return Comparison(self.dtype, self.count, rel, self.max_floored, self.max_unfloored,
+                          self.above, self.mismatch, self.zero_mismatch)
+
+
 def compare(gpu: np.ndarray, ref: np.ndarray, dtype: str) -> Comparison:
     """Compare decoded GPU values ``gpu`` with oracle values ``ref`` (both (m, n) float64)."""
-    gpu = np.asarray(gpu, dtype=np.float64)
-    ref = np.asarray(ref, dtype=np.float64)
-    if gpu.shape != ref.shape:
-        raise ValueError(f"shape mismatch {gpu.shape} vs {ref.shape}")
-    if ref.ndim == 1:
-        gpu = gpu[None, :]
-        ref = ref[None, :]
-    fin = np.isfinite(ref)
-    nan_ref = np.isnan(ref)
-    inf_ref = np.isinf(ref)
-    mismatch = int(np.count_nonzero(nan_ref & ~np.isnan(gpu)))
-    mismatch += int(np.count_nonzero(inf_ref & (gpu != ref)))
-    mismatch += int(np.count_nonzero(fin & ~np.isfinite(gpu)))
-
-    g = np.where(fin, gpu, 0.0)
-    r = np.where(fin, ref, 0.0)
-    diff = np.where(fin & np.isfinite(gpu), g - r, 0.0)
-    den = float(np.sqrt(np.sum(r * r)))
-    num = float(np.sqrt(np.sum(diff * diff)))
-    rel = num / den if den > 0 else (0.0 if num == 0 else float("inf"))
-
-    rms = np.sqrt(np.mean(r * r, axis=1, keepdims=True))
-    tau = rms * 2.0 ** FLOOR_LOG2
-    absdiff = np.abs(diff)
-    floored = absdiff / ulp(np.maximum(np.abs(r), tau), dtype)
-    unfloored = absdiff / ulp(np.abs(r), dtype)
-    zero_rows = np.all(r == 0, axis=1) & np.all(fin, axis=1)
-    zero_mismatch = int(np.count_nonzero(np.any(g[zero_rows] != 0, axis=1))) if zero_rows.any() else 0
-    floored_fin = np.where(fin, floored, 0.0)
-    unfloored_fin = np.where(fin, unfloored, 0.0)
-    return Comparison(
-        dtype=dtype,
-        count=int(ref.size),
-        rel_l2=rel,
-        max_ulp_floored=float(floored_fin.max()) if ref.size else 0.0,
-        max_ulp_unfloored=float(unfloored_fin.max()) if ref.size else 0.0,
-        n_above_4ulp_unfloored=int(np.count_nonzero(unfloored_fin > MAX_ULP_LIMIT)),
-        nonfinite_mismatch=mismatch,
-        zero_row_mismatch=zero_mismatch,
-    )
+    return Accumulator(dtype).add(gpu, ref).result()

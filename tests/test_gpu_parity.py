@@ -1,0 +1,247 @@
+"""GPU parity: libhadacore (through its C ABI) against the fp64 oracle.
+
+Tolerance (written here, derived in the design notes): rel-L2 <= 1e-3 (fp16)
+or 8e-3 (bf16) and max error <= 4 ulp of the output dtype with the ulp taken
+at max(|ref|, 2^-8 * row RMS); non-finite outputs must match by class.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from gpu_util import compare_with_oracle, say, to_device, to_host
+from metrics import bits_to_f64
+from paper_2412_08832_amd import hadacore as H
+from paper_2412_08832_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+DTYPES = ["fp16", "bf16"]
+CODE = {"fp16": H.FP16, "bf16": H.BF16}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    H.library()  # fail loudly if the HIP library is missing
+    yield
+    torch.cuda.synchronize()
+
+
+def _run(bits: np.ndarray, dtype: str, scale: float, n: int, inplace: bool,
+         out_stride: int | None = None, out_fill: int = 0xAAAA):
+    """Transform on the GPU through hadamard_transform_strided; returns output bits."""
+    import torch
+    m, in_stride = bits.shape
+    x = to_device(bits, dtype)
+    if inplace:
+        out, out_stride = x, in_stride
+    else:
+        out_stride = n if out_stride is None else out_stride
+        out = to_device(np.full((m, out_stride), out_fill, np.uint16), dtype)
+    H.hadamard_transform_strided(x.data_ptr(), in_stride, out.data_ptr(), out_stride, m, n,
+                                 CODE[dtype], scale, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    return to_host(out)
+
+
+def _ragged_rows(L: int) -> int:
+    # small n: many 4-wave workgroups plus a ragged tail; large n: one row per workgroup
+    return (1 << 21 >> L) + 3 if L <= 12 else 37
+
+
+@pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", range(7, 16))
+def test_every_size_ragged(oracle, L, dtype, inplace):
+    n = 1 << L
+    m = _ragged_rows(L)
+    say(f"every_size n={n} m={m} {dtype} inplace={inplace}")
+    bits = W.random_rows(m, n, dtype, seed=1000 + L)
+    s = W.default_scale(n)
+    out = _run(bits, dtype, s, n, inplace)
+    c = compare_with_oracle(oracle, out, bits, dtype, s, n)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4"])
+def test_configs_full_size(oracle, name):
+    w = W.CONFIGS[name]
+    say(f"config {w.name}: {w.description}")
+    bits = W.generate(w)
+    out = _run(bits, w.dtype, w.scale, w.n, w.inplace)
+    c = compare_with_oracle(oracle, out, bits, w.dtype, w.scale, w.n)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", range(7, 16))
+def test_sweep_full_size_sampled(oracle, L, dtype):
+    w = W.sweep_point(L, dtype, inplace=True)
+    say(f"sweep {w.name} (sampled rows)")
+    bits = W.generate(w)
+    out = _run(bits, dtype, w.scale, w.n, True)
+    rng = np.random.default_rng(L)
+    rows = np.unique(np.r_[0, w.m - 1, rng.integers(0, w.m, 256)])
+    c = compare_with_oracle(oracle, out, bits, dtype, w.scale, w.n, rows=rows)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", [7, 8, 11, 12, 13, 15])
+def test_single_row(oracle, L, dtype):
+    n = 1 << L
+    bits = W.random_rows(1, n, dtype, seed=7 + L)
+    out = _run(bits, dtype, 0.5, n, False)
+    c = compare_with_oracle(oracle, out, bits, dtype, 0.5, n)
+    assert c.ok, str(c)
+
+
+def test_zero_rows_leaves_output_untouched():
+    import torch
+    x = to_device(np.full((4, 256), 0x3C00, np.uint16), "fp16")
+    H.hadamard_transform(x.data_ptr(), x.data_ptr(), 0, 256, H.FP16, 1.0,
+                         torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert (to_host(x) == 0x3C00).all()
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", [7, 9, 12, 14])
+def test_strided_rows_keep_gaps(oracle, L, dtype):
+    n = 1 << L
+    m = 19
+    in_stride, out_stride = n + 24, n + 40
+    bits = W.random_rows(m, n, dtype, seed=L, stride=in_stride, fill_bits=0x7FC1)
+    s = W.default_scale(n)
+    out = _run(bits, dtype, s, n, False, out_stride=out_stride, out_fill=0x5A5A)
+    assert (out[:, n:] == 0x5A5A).all(), "out-of-place write touched the row gap"
+    c = compare_with_oracle(oracle, out, bits, dtype, s, n)
+    assert c.ok, str(c)
+    # in place on the strided buffer: gap canaries stay, rows transform
+    out2 = _run(bits, dtype, s, n, True)
+    assert (out2[:, n:] == 0x7FC1).all(), "in-place write touched the row gap"
+    assert np.array_equal(out2[:, :n], out[:, :n])
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_large_offsets(oracle, dtype):
+    """Rows 512 MiB apart: byte offsets beyond 2^31 must address correctly."""
+    import torch
+    n, m, stride = 256, 5, 1 << 28
+    say(f"large offsets {dtype}: 5 rows, stride 2^28 elements")
+    buf = torch.zeros(m * stride, dtype=torch.int16, device="cuda")
+    bits = W.random_rows(m, n, dtype, seed=77)
+    for i in range(m):
+        buf[i * stride:i * stride + n] = torch.from_numpy(bits[i].view(np.int16)).cuda()
+    x = buf.view(torch.float16 if dtype == "fp16" else torch.bfloat16)
+    s = W.default_scale(n)
+    H.hadamard_transform_strided(x.data_ptr(), stride, x.data_ptr(), stride, m, n, CODE[dtype],
+                                 s, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    out = np.stack([buf[i * stride:i * stride + n].cpu().numpy().view(np.uint16) for i in range(m)])
+    c = compare_with_oracle(oracle, out, bits, dtype, s, n)
+    assert c.ok, str(c)
+    del buf
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", [7, 10, 13, 15])
+def test_special_vectors(L, dtype):
+    n = 1 << L
+    one = W.round_to_bits(np.array([1.0], np.float32), dtype)[0]
+    rows = np.zeros((4, n), np.uint16)
+    rows[0, 0] = one                       # delta -> all ones
+    rows[1, :] = one                       # ones -> n e_0
+    k = n // 2 + 5                         # a Walsh row -> n e_k
+    parity = np.array([bin(k & j).count("1") & 1 for j in range(n)])
+    rows[2] = W.round_to_bits(np.where(parity == 1, -1.0, 1.0).astype(np.float32), dtype)
+    # row 3 stays zero
+    s = 2.0 ** -(L // 2)
+    out = bits_to_f64(_run(rows, dtype, s, n, False), dtype)
+    assert np.array_equal(out[0], np.full(n, s))
+    e0 = np.zeros(n)
+    e0[0] = n * s
+    assert np.array_equal(out[1], e0)
+    ek = np.zeros(n)
+    ek[k] = n * s
+    assert np.array_equal(out[2], ek)
+    assert np.array_equal(out[3], np.zeros(n))
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", [7, 12, 15])
+def test_nonfinite_and_subnormal_inputs(oracle, L, dtype):
+    n = 1 << L
+    bits = W.random_rows(6, n, dtype, seed=3)
+    nan = 0x7E00 if dtype == "fp16" else 0x7FC0
+    inf = 0x7C00 if dtype == "fp16" else 0x7F80
+    bits[0, n // 3] = nan
+    bits[1, 5] = inf
+    bits[2, 1] = inf
+    bits[2, n - 2] = inf | 0x8000
+    # row 3: subnormals only
+    rng = np.random.default_rng(5)
+    sub = rng.integers(1, 0x3FF if dtype == "fp16" else 0x7F, n).astype(np.uint16)
+    bits[3] = sub | (rng.integers(0, 2, n).astype(np.uint16) << 15)
+    s = W.default_scale(n)
+    out = _run(bits, dtype, s, n, False)
+    c = compare_with_oracle(oracle, out, bits, dtype, s, n)
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("L", [7, 12, 15])
+def test_bf16_huge_values_do_not_overflow(oracle, L):
+    n = 1 << L
+    rng = np.random.default_rng(L)
+    vals = (rng.choice([-1.0, 1.0], (8, n)) * rng.uniform(1e36, 3e37, (8, n))).astype(np.float32)
+    bits = W.round_to_bits(vals, "bf16")
+    s = W.default_scale(n)
+    out = _run(bits, "bf16", s, n, False)
+    assert np.isfinite(bits_to_f64(out, "bf16")).all()
+    c = compare_with_oracle(oracle, out, bits, "bf16", s, n)
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", range(7, 16))
+def test_deterministic_and_inplace_equals_out_of_place(L, dtype):
+    n = 1 << L
+    m = 4096 >> max(0, L - 10) if L <= 12 else 9
+    bits = W.random_rows(m, n, dtype, seed=L + 50)
+    s = W.default_scale(n)
+    a = _run(bits, dtype, s, n, False)
+    b = _run(bits, dtype, s, n, False)
+    c = _run(bits, dtype, s, n, True)
+    assert np.array_equal(a, b)
+    assert np.array_equal(a, c)
+
+
+def test_python_wrapper_errors_and_stream():
+    import torch
+    x = torch.randn(64, 256, device="cuda").to(torch.float16)
+    with pytest.raises(TypeError):
+        H.transform(x.float())
+    with pytest.raises(ValueError):
+        H.transform(x.t())
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        y = H.transform(x)
+    side.synchronize()
+    ref = H.transform(x)
+    torch.cuda.synchronize()
+    assert torch.equal(y, ref)
+
+
+def test_stream_copy():
+    import torch
+    src = torch.randint(-30000, 30000, (1 << 22,), dtype=torch.int16, device="cuda")
+    dst = torch.zeros_like(src)
+    H.hadacore_stream_copy(src.data_ptr(), dst.data_ptr(), src.numel() * 2,
+                           torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert torch.equal(src, dst)
