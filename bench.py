@@ -175,9 +175,15 @@ def cpu_baseline(w, target_seconds: float) -> dict:
     rate = probe_rows * w.n / max(time.perf_counter() - t0, 1e-6)
     rows = int(min(w.m, max(probe_rows, target_seconds * rate / w.n)))
     bits = W.generate(w, rows=rows) if rows != probe_rows else bits
+    # repeat the pass when the whole sample is shorter than the target duration
+    passes = 0
     t0 = time.perf_counter()
-    orc.fwht(bits, w.dtype, w.scale, nthreads=cores)
-    sec = time.perf_counter() - t0
+    while True:
+        orc.fwht(bits, w.dtype, w.scale, nthreads=cores)
+        passes += 1
+        sec = time.perf_counter() - t0
+        if sec >= target_seconds or passes >= 1000:
+            break
     cpu = ""
     try:
         for line in Path("/proc/cpuinfo").read_text().splitlines():
@@ -187,8 +193,9 @@ def cpu_baseline(w, target_seconds: float) -> dict:
     except OSError:
         pass
     return {
-        "value": rows * w.n / sec, "unit": "elements/s", "cores": cores, "kind": "oracle",
-        "sample": f"first {rows} of {w.m} rows ({rows * w.n} elements), {sec:.1f} s, "
+        "value": passes * rows * w.n / sec, "unit": "elements/s", "cores": cores, "kind": "oracle",
+        "sample": f"{passes} pass(es) over the first {rows} of {w.m} rows ({rows * w.n} "
+                  f"elements each), {sec:.1f} s, "
                   f"fp64 iterative FWHT in C on {cores} threads, {cpu}",
     }
 
