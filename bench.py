@@ -38,8 +38,10 @@ PROFILES = ROOT / "profiles"
 def parse_args(argv=None):
     p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=5)
+    # the GPU needs ~10 ms of sustained load to reach its steady clock; the
+    # defaults warm up past that and time ~20 ms of back-to-back calls
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=100)
     p.add_argument("--workload", default="c2", help="c1, c2, c3, c4 or sweep:<dtype>:<log2 n>:<in|out>")
     p.add_argument("--sweep", metavar="FILE", help="also time every workload, one JSON line each")
     p.add_argument("--cpu-seconds", type=float, default=10.0,

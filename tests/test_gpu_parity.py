@@ -47,7 +47,8 @@ def _run(bits: np.ndarray, dtype: str, scale: float, n: int, inplace: bool,
 
 
 def _ragged_rows(L: int) -> int:
-    # small n: many 4-wave workgroups plus a ragged tail; large n: one row per workgroup
+    # n <= 4096 spans many workgroups and leaves a ragged tail (multi-row tiles for
+    # n <= 256); larger n run one row per workgroup
     return (1 << 21 >> L) + 3 if L <= 12 else 37
 
 
