@@ -42,7 +42,8 @@ def parse_args(argv=None):
     # defaults warm up past that and time ~20 ms of back-to-back calls
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=100)
-    p.add_argument("--workload", default="c2", help="c1, c2, c3, c4 or sweep:<dtype>:<log2 n>:<in|out>")
+    p.add_argument("--workload", default="bf16_1048576x128_inplace",
+                   help="a named workload (workloads.WORKLOADS) or sweep:<dtype>:<log2 n>:<in|out>")
     p.add_argument("--sweep", metavar="FILE", help="also time every workload, one JSON line each")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="target duration of the CPU oracle baseline sample")
@@ -52,8 +53,8 @@ def parse_args(argv=None):
 
 def workload_by_name(name: str):
     from paper_2412_08832_amd import workloads as W
-    if name in W.CONFIGS:
-        return W.CONFIGS[name]
+    if name in W.WORKLOADS:
+        return W.WORKLOADS[name]
     m = re.fullmatch(r"sweep:(fp16|bf16):(\d+):(in|out)", name)
     if not m:
         raise SystemExit(f"unknown workload {name!r}")
@@ -239,7 +240,7 @@ def main(argv=None) -> int:
     }
     if args.sweep:
         from paper_2412_08832_amd import workloads as W
-        points = [W.CONFIGS[k] for k in ("c1", "c2", "c3", "c4")]
+        points = [W.WORKLOADS[k] for k in ("fp16_1024x256", "bf16_1048576x128_inplace", "fp16_16384x4096", "bf16_4096x32768_inplace")]
         for inplace in (True, False):
             for dt in ("fp16", "bf16"):
                 points += [W.sweep_point(k, dt, inplace) for k in range(7, 16)]

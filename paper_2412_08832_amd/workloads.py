@@ -80,29 +80,30 @@ class Workload:
     description: str
 
 
-def _c1() -> Workload:
-    return Workload("c1_fp16_1024x256", FP16, 1024, 256, False, 1.0 / 16,
+def _fp16_1024x256() -> Workload:
+    return Workload("fp16_1024x256", FP16, 1024, 256, False, 1.0 / 16,
                     "fp16 1024x256, N(0,1) seed 0, out-of-place, scale 1/16")
 
 
-def _c2() -> Workload:
-    return Workload("c2_bf16_1048576x128_inplace", BF16, 1 << 20, 128, True, default_scale(128),
+def _bf16_1048576x128_inplace() -> Workload:
+    return Workload("bf16_1048576x128_inplace", BF16, 1 << 20, 128, True, default_scale(128),
                     "bf16 head_dim rotation: 8x32x4096 rows of 128, N(0,1) with 0.1% of entries "
                     "x100, in-place, scale fp32(1/sqrt(128))")
 
 
-def _c3() -> Workload:
-    return Workload("c3_fp16_16384x4096", FP16, 16384, 4096, False, 1.0 / 64,
+def _fp16_16384x4096() -> Workload:
+    return Workload("fp16_16384x4096", FP16, 16384, 4096, False, 1.0 / 64,
                     "fp16 hidden-dim rotation 16384x4096, N(0,1) with 16 fixed columns x50, "
                     "out-of-place, scale 1/64")
 
 
-def _c4() -> Workload:
-    return Workload("c4_bf16_4096x32768_inplace", BF16, 4096, 32768, True, default_scale(32768),
+def _bf16_4096x32768_inplace() -> Workload:
+    return Workload("bf16_4096x32768_inplace", BF16, 4096, 32768, True, default_scale(32768),
                     "bf16 largest size 4096x32768, U(-1,1), in-place, scale fp32(1/sqrt(32768))")
 
 
-CONFIGS = {"c1": _c1(), "c2": _c2(), "c3": _c3(), "c4": _c4()}
+WORKLOADS = {w.name: w for w in (_fp16_1024x256(), _bf16_1048576x128_inplace(), _fp16_16384x4096(),
+                                  _bf16_4096x32768_inplace())}
 
 
 def sweep_point(k: int, dtype: str, inplace: bool, total_log2: int = 28) -> Workload:
@@ -125,26 +126,26 @@ def generate(w: Workload, rows: int | None = None) -> np.ndarray:
     """The workload's input bits, (m, n) uint16.
 
     ``rows`` keeps only the first rows.  numpy fills draws in row-major order, so
-    a draw of fewer rows equals the first rows of the full draw; the c2 recipe
-    draws its outlier mask after all values and therefore always draws in full.
+    a draw of fewer rows equals the first rows of the full draw; the
+    bf16_1048576x128_inplace recipe draws its outlier mask after all values and therefore always draws in full.
     """
     m = w.m if rows is None else min(int(rows), w.m)
     n = w.n
-    if w.name.startswith("c1"):
+    if w.name == "fp16_1024x256":
         rng = np.random.default_rng(0)
         vals = rng.standard_normal((m, n), dtype=np.float32)
-    elif w.name.startswith("c2"):
+    elif w.name == "bf16_1048576x128_inplace":
         rng = np.random.default_rng(2)
         vals = rng.standard_normal((w.m, n), dtype=np.float32)
         mask = rng.random((w.m, n), dtype=np.float32) < 1e-3
         vals[mask] *= np.float32(100.0)
         vals = vals[:m]
-    elif w.name.startswith("c3"):
+    elif w.name == "fp16_16384x4096":
         rng = np.random.default_rng(3)
         cols = rng.choice(n, 16, replace=False)
         vals = rng.standard_normal((m, n), dtype=np.float32)
         vals[:, cols] *= np.float32(50.0)
-    elif w.name.startswith("c4"):
+    elif w.name == "bf16_4096x32768_inplace":
         rng = np.random.default_rng(4)
         vals = rng.uniform(-1.0, 1.0, (m, n)).astype(np.float32)
     elif w.name.startswith("sweep"):
@@ -156,6 +157,6 @@ def generate(w: Workload, rows: int | None = None) -> np.ndarray:
     return round_to_bits(np.ascontiguousarray(vals), w.dtype)
 
 
-def c3_outlier_columns() -> np.ndarray:
-    """The 16 columns scaled x50 in the c3 workload (drawn first from seed 3)."""
+def hidden_outlier_columns() -> np.ndarray:
+    """The 16 columns scaled x50 in the fp16_16384x4096 workload (drawn first from seed 3)."""
     return np.sort(np.random.default_rng(3).choice(4096, 16, replace=False))

@@ -67,9 +67,9 @@ def test_every_size_ragged(oracle, L, dtype, inplace):
     assert c.ok, str(c)
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4"])
+@pytest.mark.parametrize("name", ["fp16_1024x256", "bf16_1048576x128_inplace", "fp16_16384x4096", "bf16_4096x32768_inplace"])
 def test_configs_full_size(oracle, name):
-    w = W.CONFIGS[name]
+    w = W.WORKLOADS[name]
     say(f"config {w.name}: {w.description}")
     bits = W.generate(w)
     out = _run(bits, w.dtype, w.scale, w.n, w.inplace)

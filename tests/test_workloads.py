@@ -31,18 +31,18 @@ def test_fp16_rounding_is_numpy_rne():
 
 
 def test_truncated_draw_is_prefix_of_full_draw():
-    for w in (W.CONFIGS["c1"], W.CONFIGS["c3"], W.sweep_point(12, "bf16", True)):
+    for w in (W.WORKLOADS["fp16_1024x256"], W.WORKLOADS["fp16_16384x4096"], W.sweep_point(12, "bf16", True)):
         small = W.generate(w, rows=5)
         # the full recipe at a reduced row count must start with the same rows
         bigger = W.generate(w, rows=9)
         assert np.array_equal(small, bigger[:5])
 
 
-def test_c2_outliers_and_c3_columns():
-    w2 = W.CONFIGS["c2"]
+def test_outlier_workloads():
+    w2 = W.WORKLOADS["bf16_1048576x128_inplace"]
     assert (w2.m, w2.n, w2.inplace) == (1 << 20, 128, True)
-    x3 = W.generate(W.CONFIGS["c3"], rows=64).view(np.float16).astype(np.float64)
-    cols = W.c3_outlier_columns()
+    x3 = W.generate(W.WORKLOADS["fp16_16384x4096"], rows=64).view(np.float16).astype(np.float64)
+    cols = W.hidden_outlier_columns()
     assert len(cols) == 16
     big = np.abs(x3[:, cols]).mean()
     rest = np.abs(np.delete(x3, cols, axis=1)).mean()
