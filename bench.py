@@ -39,9 +39,9 @@ def parse_args(argv=None):
     p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     p.add_argument("--gpus", type=int, default=1)
     # the GPU needs ~10 ms of sustained load to reach its steady clock; the
-    # defaults warm up past that and time ~20 ms of back-to-back calls
+    # defaults warm up for ~25 ms and time ~17 ms of back-to-back calls
     p.add_argument("--steps", type=int, default=200)
-    p.add_argument("--warmup", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=300)
     p.add_argument("--workload", default="bf16_1048576x128_inplace",
                    help="a named workload (workloads.WORKLOADS) or sweep:<dtype>:<log2 n>:<in|out>")
     p.add_argument("--sweep", metavar="FILE", help="also time every workload, one JSON line each")
@@ -100,12 +100,18 @@ class Device:
         t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(self.dev)
         return t.view(torch.float16 if dtype == "fp16" else torch.bfloat16)
 
-    def time_calls(self, calls, steps: int, warmup: int) -> float:
+    def time_calls(self, calls, steps: int, warmup: int, min_warm_s: float = 0.0) -> float:
         """Seconds for `steps` back-to-back calls (cycling through `calls`), HIP events
-        recorded on the stream the kernels are launched on."""
+        recorded on the stream the kernels are launched on.  At least `warmup` untimed
+        calls run first, and more until `min_warm_s` seconds of them have run."""
         torch = self.torch
-        for i in range(warmup):
+        t0 = time.perf_counter()
+        i = 0
+        while i < warmup or (min_warm_s > 0 and time.perf_counter() - t0 < min_warm_s):
             calls[i % len(calls)]()
+            i += 1
+            if min_warm_s > 0 and i % 50 == 0:
+                torch.cuda.synchronize(self.dev)
         torch.cuda.synchronize(self.dev)
         start = torch.cuda.Event(enable_timing=True)
         end = torch.cuda.Event(enable_timing=True)
@@ -118,7 +124,7 @@ class Device:
         return start.elapsed_time(end) / 1e3
 
 
-def time_workload(d: Device, w, steps: int, warmup: int) -> dict:
+def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0) -> dict:
     from paper_2412_08832_amd import workloads as W
     H, torch = d.H, d.torch
     bits = W.generate(w)
@@ -136,7 +142,7 @@ def time_workload(d: Device, w, steps: int, warmup: int) -> dict:
                                           w.scale, s))
         for i in range(nbuf)
     ]
-    sec = d.time_calls(calls, steps, warmup)
+    sec = d.time_calls(calls, steps, warmup, min_warm_s)
     per_launch = sec / steps
     alg_bytes = 2 * nbytes                      # one read + one write of every element
     gbs = alg_bytes / per_launch / 1e9
@@ -148,7 +154,7 @@ def time_workload(d: Device, w, steps: int, warmup: int) -> dict:
         (lambda i=i: H.hadacore_stream_copy(srcs[i].data_ptr(), dsts[i].data_ptr(), nbytes, s))
         for i in range(nbuf)
     ]
-    csec = d.time_calls(copies, steps, warmup) / steps
+    csec = d.time_calls(copies, steps, warmup, min_warm_s) / steps
     copy_gbs = alg_bytes / csec / 1e9
     del ins, outs, srcs, dsts, first
     torch.cuda.empty_cache()
@@ -246,7 +252,7 @@ def main(argv=None) -> int:
                 points += [W.sweep_point(k, dt, inplace) for k in range(7, 16)]
         with open(args.sweep, "w") as f:
             for p in points:
-                pr = time_workload(d, p, args.steps, args.warmup)
+                pr = time_workload(d, p, args.steps, args.warmup, min_warm_s=0.03)
                 f.write(json.dumps(pr) + "\n")
                 f.flush()
                 print(f"[sweep] {p.name}: {pr['gbs']:.0f} GB/s ({100 * pr['frac_hbm_peak']:.1f}% "

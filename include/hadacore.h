@@ -13,10 +13,11 @@
  * stored.  n is a power of two from 2^7 to 2^15 (Sec. 2.3-2.4 and Sec. 3.2
  * bound the sizes at 2^15).  In-place operation (Appendix B) is supported.
  *
- * Numerics: inputs are widened exactly to fp32, multiplied by `scale` once
- * (before the butterflies, so that large bf16 rows cannot overflow fp32
- * partial sums), transformed with fp32 intermediates only, and rounded once
- * to the output dtype with round-to-nearest-even.  Subnormals are preserved.
+ * Numerics: inputs are scaled before any addition -- by `scale`, or by its
+ * power-of-two part with the remaining factor (in [1, 2)) applied at the end --
+ * so that large bf16 rows cannot overflow fp32 partial sums; all intermediates
+ * are fp32 and the result is rounded once to the output dtype with
+ * round-to-nearest-even.  Subnormals are preserved.
  * NaN/Inf propagate as IEEE arithmetic dictates.  Results are deterministic:
  * repeated calls, and in-place vs out-of-place calls, give identical bits.
  *
@@ -29,6 +30,13 @@
  * means the default stream) and the call returns without synchronizing.
  * Buffers must stay alive until that work completes.  Faults in the enqueued
  * kernel surface at the caller's next synchronization, not here.
+ *
+ * Kernels: per transform size the library picks one of two front ends for the
+ * first stages, both giving results within fp32 rounding of each other: fp32
+ * VALU butterflies, or one radix-32 step on the matrix cores (MFMA) applied
+ * directly to the 16-bit inputs.  The environment variable HADACORE_VARIANT
+ * set to "valu" or "mfma" forces one of them (testing and tuning; read on
+ * every call); unset keeps the measured per-size choice.
  *
  * Errors: arguments are validated synchronously before anything is enqueued;
  * on error nothing is enqueued and a nonzero status is returned.  No call

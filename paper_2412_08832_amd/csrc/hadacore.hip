@@ -32,20 +32,29 @@
 // The negation is tracked per lane (it depends only on which lane bits were
 // processed) and undone by flipping sign bits of the packed 16-bit results.
 //
-// Numerics: inputs are widened exactly and multiplied by the scale before
-// any addition (folded into the first butterfly), so large bf16 rows do not
-// overflow fp32 partial sums; every intermediate is fp32 and the result is
-// rounded once, round-to-nearest-even.
+// Two front ends do the first stages on the raw 16-bit data (see "front
+// ends" below): fp32 VALU butterflies, or one radix-32 step as a pair of
+// MFMA 16x16x32 products -- the paper's Tensor-Core idea (Sec. 3) on CDNA4
+// matrix cores, applied to the exact 16-bit inputs only.  Per size the
+// dispatcher uses whichever measured faster.
 //
-// Where this differs from the paper's kernel: the paper maps 16-point
-// transforms onto 16x16 Tensor-Core matmuls (Sec. 3) and keeps fp16/bf16
-// intermediates; here the stages are fp32 VALU butterflies with wave64 DPP
-// and LDS exchanges, which keeps one rounding and is bound by HBM bandwidth.
+// Numerics: inputs are scaled before any addition (the VALU front multiplies
+// while widening; the MFMA front puts the power-of-two part of the scale into
+// its H_32 operand and applies the rest at the end), so large bf16 rows do
+// not overflow fp32 partial sums.  Every intermediate is fp32 and the result
+// is rounded once, round-to-nearest-even.
+//
+// Where this differs from the paper's kernel: the paper chains 16x16
+// Tensor-Core products with fp16/bf16 intermediates and transposes between
+// them (Sec. 3.1-3.2); here only the first step may use the matrix cores,
+// everything after it is fp32 VALU butterflies with wave64 DPP and LDS
+// exchanges, which keeps one rounding, and the kernel is HBM-bound.
 
 #include <hip/hip_runtime.h>
 
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <atomic>
@@ -59,6 +68,9 @@ typedef float f2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 
 constexpr int kWave = 64;
 
@@ -188,21 +200,73 @@ __device__ __forceinline__ void lane_stage(float (&v)[N], int lane) {
   }
 }
 
-// Lane bits of a wave that carry element bits for rows of 2^L elements.
+// ---- front ends: the stages applied to the raw 16-bit data ----------------------
+//
+// kValu: each lane widens its 16-byte chunk (8 consecutive elements) to fp32,
+//   multiplies by the scale and runs the butterflies on element bits 0-2 in
+//   registers; lane l holds tile bits 3-8 equal to l.
+// kMfma: the radix-32 step on tile bits 0-4 is one pair of 16x16x32 MFMAs on
+//   the raw 16-bit data (the Tensor-Core idea of the paper's Sec. 3, as a
+//   32-point product on CDNA4 matrix cores).  Lane l loads chunk (l >> 4) of
+//   the 32-element vector pi(l & 15) -- exactly the MFMA B-operand layout --
+//   and the A operands are the top and bottom 16 rows of H_32 times 2^e, which
+//   are exact in 16 bits.  The fp32 products come back as element 4(l>>4)+i
+//   and 16+4(l>>4)+i of the lane's vector; one v_permlane16_swap per register
+//   pair turns that into 8 consecutive elements, 8*hsel(l >> 4) onwards, so
+//   stores stay 16 bytes per lane.  What remains are the vector bits (tile
+//   bits 5-8, on lane bits 0-3) and the chunk and wave bits; the result is
+//   multiplied by scale / 2^e at the end.
+constexpr int kValu = 0;
+constexpr int kMfma = 1;
+
+// Vector index (tile bits 5-8) held by lane l in the MFMA layout.  For n = 256
+// the vector's third bit sits on lane bit 3 so that all three element-carrying
+// lane bits are DPP lanes (xor 1, 2, 8); otherwise the identity.
 template <int L>
-constexpr int lane_bits() {
-  return L - 3 >= 6 ? 6 : L - 3;
+__device__ __forceinline__ int mfma_vector(int l) {
+  l &= 15;
+  if constexpr (L == 8) l = (l & 3) | ((l & 4) << 1) | ((l & 8) >> 1);
+  return l;
 }
 
-// Sign-flip mask for the packed results of this lane: a lane holds negated
-// values iff an odd number of its processed lane bits are set.
-template <int L>
-__device__ __forceinline__ uint32_t twist_flip(int lane) {
-  const int processed = lane & ((1 << lane_bits<L>()) - 1);
-  return (__builtin_popcount(processed) & 1) ? 0x80008000u : 0u;
+// Tile bits 3-8 of the chunk lane l loads / holds after the front end.
+template <int FRONT, int L>
+__device__ __forceinline__ int lane_field_load(int l) {
+  if constexpr (FRONT == kValu) {
+    return l;
+  } else {
+    return 4 * mfma_vector<L>(l) + (l >> 4);
+  }
 }
 
-// Widen + scale + stage on bit 0 for all registers.
+template <int FRONT, int L>
+__device__ __forceinline__ int lane_field(int l) {
+  if constexpr (FRONT == kValu) {
+    return l;
+  } else {
+    const int g = l >> 4;
+    return 4 * mfma_vector<L>(l) + (((g & 1) << 1) | (g >> 1));  // hsel = {0, 2, 1, 3}
+  }
+}
+
+// Lane bits that carry element bits still to be processed after the front end
+// (a mask over lane bits 0-5).
+template <int FRONT, int L>
+constexpr int lane_stage_mask() {
+  if constexpr (FRONT == kValu) {
+    return (1 << (L - 3 >= 6 ? 6 : L - 3)) - 1;
+  } else {
+    return L == 7 ? 0x3 : (L == 8 ? 0xB : 0xF);
+  }
+}
+
+// A lane holds negated values iff an odd number of its processed lane bits are set.
+template <int FRONT, int L>
+__device__ __forceinline__ bool twisted(int lane) {
+  return (__builtin_popcount(lane & lane_stage_mask<FRONT, L>()) & 1) != 0;
+}
+
+// Widen + scale + stage on bit 0 for all registers (kValu front).
 template <int DT, int C>
 __device__ __forceinline__ void widen_chunks(const u4 (&raw)[C], float (&v)[C * 8], float s) {
 #pragma unroll
@@ -216,77 +280,195 @@ __device__ __forceinline__ void widen_chunks(const u4 (&raw)[C], float (&v)[C * 
   }
 }
 
-// Every stage whose bit lies inside one wave except element bit 0 (done while
-// widening): in-chunk bits 1-2, the chunk bits that are element bits (tile
-// bits 9.. below L), and the lane bits (tile bits 3-8) below L.
-template <int L, int C, int N>
+// MFMA A operand for lane l: 8 consecutive 16-bit entries of row (l & 15) (top)
+// or 16 + (l & 15) (bottom) of H_32 * 2^e, columns 8*(l >> 4) .. +7.
+// H_32[r][c] = (-1)^popcount(r & c); bf16 entries carry 2^e in their exponent.
+template <int DT>
+__device__ __forceinline__ u4 h32_operand(int lane, int e2, int bottom) {
+  const int m = lane & 15;
+  const int g = lane >> 4;
+  const int base = (__builtin_popcount(m & (8 * g)) + (bottom & (g >> 1))) & 1;
+  const uint32_t one = DT == HADACORE_FP16 ? 0x3C00u : (uint32_t)(0x3F80 + e2 * 128);
+  u4 r;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t s0 = (uint32_t)(base ^ __builtin_popcount(m & (2 * q))) & 1u;
+    const uint32_t s1 = (uint32_t)(base ^ __builtin_popcount(m & (2 * q + 1))) & 1u;
+    r[q] = (one | (s0 << 15)) | ((one | (s1 << 15)) << 16);
+  }
+  return r;
+}
+
+// Radix-32 step of one chunk on the matrix cores (kMfma front).
+template <int DT>
+__device__ __forceinline__ void mfma_front(u4 raw, u4 a_top, u4 a_bot, float *v) {
+  const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+  f4 top, bot;
+  if constexpr (DT == HADACORE_FP16) {
+    top = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, a_top),
+                                                 __builtin_bit_cast(h8, raw), zero, 0, 0, 0);
+    bot = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, a_bot),
+                                                 __builtin_bit_cast(h8, raw), zero, 0, 0, 0);
+  } else {
+    top = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, a_top),
+                                                  __builtin_bit_cast(bf8, raw), zero, 0, 0, 0);
+    bot = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, a_bot),
+                                                  __builtin_bit_cast(bf8, raw), zero, 0, 0, 0);
+  }
+  // Bit-cast whole vectors: __builtin_bit_cast of a single ext-vector element
+  // reads element 0 in this compiler.
+  const u4 tu = __builtin_bit_cast(u4, top);
+  const u4 bu = __builtin_bit_cast(u4, bot);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const auto s = __builtin_amdgcn_permlane16_swap(tu[i], bu[i], false, false);
+    v[i] = __builtin_bit_cast(float, (uint32_t)s[0]);
+    v[4 + i] = __builtin_bit_cast(float, (uint32_t)s[1]);
+  }
+}
+
+// The front end for all chunks of a lane.
+template <int DT, int FRONT, int C>
+__device__ __forceinline__ void front(const u4 (&raw)[C], float (&v)[C * 8], int lane, float scale,
+                                      int e2) {
+  if constexpr (FRONT == kValu) {
+    widen_chunks<DT, C>(raw, v, scale);
+    reg_stage<1>(v);
+    reg_stage<2>(v);
+  } else {
+    const u4 a_top = h32_operand<DT>(lane, e2, 0);
+    const u4 a_bot = h32_operand<DT>(lane, e2, 1);
+#pragma unroll
+    for (int k = 0; k < C; ++k) mfma_front<DT>(raw[k], a_top, a_bot, &v[k * 8]);
+  }
+}
+
+// The remaining stages inside one wave: the chunk bits that are element bits
+// (tile bits 9.. below L) and the lane bits that still carry element bits.
+template <int FRONT, int L, int C, int N>
 __device__ __forceinline__ void wave_stages(float (&v)[N], int lane) {
-  reg_stage<1>(v);
-  reg_stage<2>(v);
   static_assert(C == 1 || C == 2 || C == 4 || C == 8, "1, 2, 4 or 8 chunks per lane");
   if constexpr (C >= 2 && L > 9) reg_stage<3>(v);
   if constexpr (C >= 4 && L > 10) reg_stage<4>(v);
   if constexpr (C >= 8 && L > 11) reg_stage<5>(v);
-  if constexpr (L > 3) lane_stage<0>(v, lane);
-  if constexpr (L > 4) lane_stage<1>(v, lane);
-  if constexpr (L > 5) lane_stage<2>(v, lane);
-  if constexpr (L > 6) lane_stage<3>(v, lane);
-  if constexpr (L > 7) lane_stage<4>(v, lane);
-  if constexpr (L > 8) lane_stage<5>(v, lane);
+  constexpr int mask = lane_stage_mask<FRONT, L>();
+  if constexpr (mask & 1) lane_stage<0>(v, lane);
+  if constexpr (mask & 2) lane_stage<1>(v, lane);
+  if constexpr (mask & 4) lane_stage<2>(v, lane);
+  if constexpr (mask & 8) lane_stage<3>(v, lane);
+  if constexpr (mask & 16) lane_stage<4>(v, lane);
+  if constexpr (mask & 32) lane_stage<5>(v, lane);
 }
 
-template <int DT>
-__device__ __forceinline__ u4 narrow_chunk(const float *v, uint32_t flip) {
-  u4 r;
-  r.x = narrow<DT>(v[0], v[1], flip);
-  r.y = narrow<DT>(v[2], v[3], flip);
-  r.z = narrow<DT>(v[4], v[5], flip);
-  r.w = narrow<DT>(v[6], v[7], flip);
-  return r;
-}
+// Undo the twist (and, for kMfma, apply the part of the scale the front end
+// left out), round once and pack 8 elements.
+template <int DT, int FRONT>
+struct Finisher {
+  uint32_t flip;
+  float post;
+  __device__ __forceinline__ Finisher(bool tw, float post_scale) {
+    if constexpr (FRONT == kValu) {
+      flip = tw ? 0x80008000u : 0u;
+      post = 1.0f;
+    } else {
+      flip = 0u;
+      post = tw ? -post_scale : post_scale;
+    }
+  }
+  __device__ __forceinline__ u4 operator()(const float *v) const {
+    float w[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[i] = FRONT == kValu ? v[i] : v[i] * post;
+    u4 r;
+    r.x = narrow<DT>(w[0], w[1], flip);
+    r.y = narrow<DT>(w[2], w[3], flip);
+    r.z = narrow<DT>(w[4], w[5], flip);
+    r.w = narrow<DT>(w[6], w[7], flip);
+    return r;
+  }
+};
+
+// Scale arguments: kValu multiplies by `scale` while widening; kMfma puts 2^e2
+// into the H_32 operand and multiplies by `post` = scale / 2^e2 at the end.
+struct ScaleArgs {
+  float scale;
+  float post;
+  int e2;
+};
 
 // ---- kernels ------------------------------------------------------------------
 
-// n <= 512*C: each wave owns a tile of 512*C elements = 512*C/n whole rows and
-// runs every stage inside the wave.  WPB independent waves per workgroup.
-// Tiles that end past row m (only the last one) mask their rows.
-template <int DT, int L, int C, int WPB, bool NT>
+// n <= 512*C: a tile of 512*C elements is 512*C/n whole rows and every stage
+// of a tile runs inside one wave.  Each wave processes T consecutive tiles,
+// loading tile t+1 while it computes tile t, so that per-wave setup (operand
+// constants, signs, addressing) is paid once per T tiles while only one or two
+// tiles per wave are in flight.  WPB independent waves per workgroup.  Only
+// the last tile can end past row m; it masks those rows.
+template <int DT, int L, int C, int T, int WPB, bool NT, int FRONT>
 __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
     const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, int64_t m,
-    float scale) {
+    ScaleArgs sc) {
   constexpr int kTile = 512 * C;
   static_assert((1 << L) <= kTile, "row does not fit a wave tile");
   constexpr int kRows = kTile >> L;
   constexpr int kMask = (1 << L) - 1;
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
-  const int64_t row0 = ((int64_t)blockIdx.x * WPB + wave) * kRows;
+  int64_t row0 = ((int64_t)blockIdx.x * WPB + wave) * (int64_t)(T * kRows);
   if (row0 >= m) return;
-  const bool full = row0 + kRows <= m;
-  const uint16_t *src = in + row0 * in_stride;
-  uint16_t *dst = out + row0 * out_stride;
-
-  u4 raw[C];
-#pragma unroll
-  for (int k = 0; k < C; ++k) {
-    const int t = (k * kWave + lane) * 8;
-    if (full || row0 + (t >> L) < m) {
-      raw[k] = gload<NT>(src + (int64_t)(t >> L) * in_stride + (t & kMask));
-    } else {
-      raw[k] = u4{0, 0, 0, 0};
-    }
+  const int lf_load = lane_field_load<FRONT, L>(lane);
+  const int lf = lane_field<FRONT, L>(lane);
+  const Finisher<DT, FRONT> fin(twisted<FRONT, L>(lane), sc.post);
+  u4 a_top = {0, 0, 0, 0}, a_bot = {0, 0, 0, 0};
+  if constexpr (FRONT == kMfma) {
+    a_top = h32_operand<DT>(lane, sc.e2, 0);
+    a_bot = h32_operand<DT>(lane, sc.e2, 1);
   }
-  float v[C * 8];
-  widen_chunks<DT, C>(raw, v, scale);
-  wave_stages<L, C>(v, lane);
-  const uint32_t flip = twist_flip<L>(lane);
+
+  auto load_tile = [&](int64_t r0, u4 (&raw)[C]) {
+    const bool full = r0 + kRows <= m;
+    const uint16_t *src = in + r0 * in_stride;
 #pragma unroll
-  for (int k = 0; k < C; ++k) {
-    const int t = (k * kWave + lane) * 8;
-    if (full || row0 + (t >> L) < m) {
-      gstore<NT>(dst + (int64_t)(t >> L) * out_stride + (t & kMask),
-                 narrow_chunk<DT>(&v[k * 8], flip));
+    for (int k = 0; k < C; ++k) {
+      const int t = (k * kWave + lf_load) * 8;
+      if (full || r0 + (t >> L) < m) {
+        raw[k] = gload<NT>(src + (int64_t)(t >> L) * in_stride + (t & kMask));
+      } else {
+        raw[k] = u4{0, 0, 0, 0};
+      }
     }
+  };
+
+  u4 next[C];
+  load_tile(row0, next);
+#pragma unroll 1
+  for (int it = 0; it < T; ++it) {
+    u4 raw[C];
+#pragma unroll
+    for (int k = 0; k < C; ++k) raw[k] = next[k];
+    const bool more = it + 1 < T && row0 + kRows < m;
+    if (more) load_tile(row0 + kRows, next);
+    float v[C * 8];
+    if constexpr (FRONT == kValu) {
+      widen_chunks<DT, C>(raw, v, sc.scale);
+      reg_stage<1>(v);
+      reg_stage<2>(v);
+    } else {
+#pragma unroll
+      for (int k = 0; k < C; ++k) mfma_front<DT>(raw[k], a_top, a_bot, &v[k * 8]);
+    }
+    wave_stages<FRONT, L, C>(v, lane);
+    const bool full = row0 + kRows <= m;
+    uint16_t *dst = out + row0 * out_stride;
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      const int t = (k * kWave + lf) * 8;
+      if (full || row0 + (t >> L) < m) {
+        gstore<NT>(dst + (int64_t)(t >> L) * out_stride + (t & kMask), fin(&v[k * 8]));
+      }
+    }
+    if (!more) break;
+    row0 += kRows;
   }
 }
 
@@ -295,10 +477,11 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
 // through LDS (fp32), then finished as register stages.  HALVES = 2 runs the
 // exchange in two passes over the two 4-element halves of each chunk, which
 // halves the LDS footprint (more workgroups per CU) at the cost of two extra
-// barriers.
-template <int DT, int L, int C, int HALVES, bool NT>
+// barriers.  The exchange keeps every value in its lane, so the lane layout
+// of the front end carries through to the store.
+template <int DT, int L, int C, int HALVES, bool NT, int FRONT>
 __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
-    const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, float scale) {
+    const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc) {
   constexpr int n = 1 << L;
   constexpr int NW = n / (512 * C);
   static_assert(NW >= 2 && NW <= C, "wave bits must fit the chunk bits");
@@ -315,11 +498,12 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   uint16_t *dst = out + row * out_stride;
 
   u4 raw[C];
+  const int lf_load = lane_field_load<FRONT, L>(lane);
 #pragma unroll
-  for (int k = 0; k < C; ++k) raw[k] = gload<NT>(src + ((w * C + k) * kWave + lane) * 8);
+  for (int k = 0; k < C; ++k) raw[k] = gload<NT>(src + ((w * C + k) * kWave + lf_load) * 8);
   float v[C * 8];
-  widen_chunks<DT, C>(raw, v, scale);
-  wave_stages<L, C>(v, lane);
+  front<DT, FRONT, C>(raw, v, lane, sc.scale, sc.e2);
+  wave_stages<FRONT, L, C>(v, lane);
 
 #pragma unroll
   for (int pass = 0; pass < HALVES; ++pass) {
@@ -353,11 +537,12 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   reg_stage<3>(v);
   if constexpr (NW >= 4) reg_stage<4>(v);
   if constexpr (NW >= 8) reg_stage<5>(v);
-  const uint32_t flip = twist_flip<L>(lane);
+  const Finisher<DT, FRONT> fin(twisted<FRONT, L>(lane), sc.post);
+  const int lf = lane_field<FRONT, L>(lane);
 #pragma unroll
   for (int k = 0; k < C; ++k) {
     const int W = (k % NW) * C + (k / NW) * NW + w;
-    gstore<NT>(dst + (W * kWave + lane) * 8, narrow_chunk<DT>(&v[k * 8], flip));
+    gstore<NT>(dst + (W * kWave + lf) * 8, fin(&v[k * 8]));
   }
 }
 
@@ -371,70 +556,101 @@ __global__ __launch_bounds__(256) void stream_copy_kernel(const uint16_t *src, u
 
 // ---- host dispatch ------------------------------------------------------------
 
-// Launch configuration of one (dtype, n).
-struct Config {
-  int chunks;     // C: 16-byte chunks per lane
-  int waves;      // WPB for the wave kernel (NW is implied by n and C)
-  int halves;     // block kernel: LDS exchange passes
-};
+// Splits the scale for the kMfma front: 2^e2 goes into the 16-bit H_32 operand
+// (a normal number in that dtype), the rest is applied at the end.  fp16 rows
+// cannot overflow fp32 (|x| <= 65504, n <= 2^15), so their operand is +-1.
+ScaleArgs split_scale(float scale, int dtype) {
+  ScaleArgs a{scale, scale, 0};
+  if (dtype == HADACORE_BF16 && scale != 0.0f) {
+    int e = 0;
+    frexpf(fabsf(scale), &e);  // |scale| = f * 2^e, f in [0.5, 1)
+    e -= 1;                    // 2^e <= |scale| < 2^(e+1)
+    if (e < -126) e = -126;
+    if (e > 127) e = 127;
+    a.e2 = e;
+    a.post = scale / ldexpf(1.0f, e);
+  }
+  return a;
+}
 
-template <int DT, int L, int C, int WPB, int HALVES>
+// C: chunks per lane; T: tiles per wave (wave kernel) ; WPB: waves per workgroup
+// (wave kernel); HALVES: LDS exchange passes (block kernel); FRONT: kValu / kMfma.
+template <int DT, int L, int C, int T, int WPB, int HALVES, int FRONT>
 hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
-                      int64_t m, float scale, hipStream_t stream) {
+                      int64_t m, const ScaleArgs &sc, hipStream_t stream) {
   if constexpr ((1 << L) <= 512 * C) {
-    constexpr int64_t rows_per_wave = (512 * C) >> L;
+    constexpr int64_t rows_per_wave = (int64_t)T * ((512 * C) >> L);
     const int64_t waves = (m + rows_per_wave - 1) / rows_per_wave;
     const int64_t blocks = (waves + WPB - 1) / WPB;
-    hipLaunchKernelGGL((fwht_wave_kernel<DT, L, C, WPB, true>), dim3((uint32_t)blocks),
-                       dim3(kWave * WPB), 0, stream, in, in_stride, out, out_stride, m, scale);
+    hipLaunchKernelGGL((fwht_wave_kernel<DT, L, C, T, WPB, true, FRONT>), dim3((uint32_t)blocks),
+                       dim3(kWave * WPB), 0, stream, in, in_stride, out, out_stride, m, sc);
   } else {
-    hipLaunchKernelGGL((fwht_block_kernel<DT, L, C, HALVES, true>), dim3((uint32_t)m),
-                       dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out, out_stride,
-                       scale);
+    hipLaunchKernelGGL((fwht_block_kernel<DT, L, C, HALVES, true, FRONT>), dim3((uint32_t)m),
+                       dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out, out_stride, sc);
   }
   return hipGetLastError();
 }
 
-// Per-size configuration, chosen from measured HBM throughput on MI355X
-// (2^28-element in-place sweeps over chunks per lane, waves per workgroup,
-// exchange passes and cache policy): the smallest per-wave footprint that
-// holds a row wins for n <= 2048; from n = 4096 on, a row is spread over
-// several waves with one LDS exchange, run in two passes where that lets two
-// or more workgroups share a CU.
+// Per-size configuration, chosen from sustained HBM throughput measured on
+// MI355X (2^28-element in-place sweeps over chunks per lane, tiles per wave,
+// exchange passes, cache policy and front end, interleaved so that every
+// candidate sees the same clock state).  The smallest per-wave footprint that
+// holds a row wins up to n = 2048; from n = 4096 a row spreads over several
+// waves with one LDS exchange.  The matrix-core front end wins from n = 2048
+// on (except 16384); below that the VALU front is as fast and simpler.
+// `front` < 0 takes the table's choice; kValu / kMfma force one front end.
 template <int DT, int L>
 hipError_t launch(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
-                  int64_t m, float scale, hipStream_t stream) {
-  //                                      C  WPB HALVES
+                  int64_t m, const ScaleArgs &sc, int front, hipStream_t stream) {
+  //                             default front       C  T  WPB HALVES
+  constexpr int kDefault = (L >= 11 && L != 14) ? kMfma : kValu;
+  const bool mfma = front < 0 ? kDefault == kMfma : front == kMfma;
+#define HC_CFG(C, T, WPB, H)                                                                     \
+  (mfma ? launch_cfg<DT, L, C, T, WPB, H, kMfma>(in, in_stride, out, out_stride, m, sc, stream)  \
+        : launch_cfg<DT, L, C, T, WPB, H, kValu>(in, in_stride, out, out_stride, m, sc, stream))
   if constexpr (L <= 9) {
-    return launch_cfg<DT, L, 1, 1, 1>(in, in_stride, out, out_stride, m, scale, stream);
+    return HC_CFG(1, 1, 1, 1);
   } else if constexpr (L == 10) {
-    return launch_cfg<DT, L, 2, 1, 1>(in, in_stride, out, out_stride, m, scale, stream);
+    return HC_CFG(2, 1, 1, 1);
   } else if constexpr (L == 11) {
-    return launch_cfg<DT, L, 4, 1, 1>(in, in_stride, out, out_stride, m, scale, stream);
+    return HC_CFG(4, 1, 1, 1);
   } else if constexpr (L == 12) {
-    return launch_cfg<DT, L, 4, 1, 1>(in, in_stride, out, out_stride, m, scale, stream);
+    return HC_CFG(4, 1, 1, 1);
   } else if constexpr (L == 13) {
-    return launch_cfg<DT, L, 4, 1, 2>(in, in_stride, out, out_stride, m, scale, stream);
+    return mfma ? launch_cfg<DT, L, 4, 1, 1, 1, kMfma>(in, in_stride, out, out_stride, m, sc, stream)
+                : launch_cfg<DT, L, 4, 1, 1, 2, kValu>(in, in_stride, out, out_stride, m, sc, stream);
   } else {
-    return launch_cfg<DT, L, 8, 1, 2>(in, in_stride, out, out_stride, m, scale, stream);
+    return HC_CFG(8, 1, 1, 2);
   }
+#undef HC_CFG
 }
 
 template <int DT>
 hipError_t launch_dt(int L, const uint16_t *in, int64_t in_stride, uint16_t *out,
-                     int64_t out_stride, int64_t m, float scale, hipStream_t stream) {
+                     int64_t out_stride, int64_t m, const ScaleArgs &sc, int front,
+                     hipStream_t stream) {
   switch (L) {
-    case 7: return launch<DT, 7>(in, in_stride, out, out_stride, m, scale, stream);
-    case 8: return launch<DT, 8>(in, in_stride, out, out_stride, m, scale, stream);
-    case 9: return launch<DT, 9>(in, in_stride, out, out_stride, m, scale, stream);
-    case 10: return launch<DT, 10>(in, in_stride, out, out_stride, m, scale, stream);
-    case 11: return launch<DT, 11>(in, in_stride, out, out_stride, m, scale, stream);
-    case 12: return launch<DT, 12>(in, in_stride, out, out_stride, m, scale, stream);
-    case 13: return launch<DT, 13>(in, in_stride, out, out_stride, m, scale, stream);
-    case 14: return launch<DT, 14>(in, in_stride, out, out_stride, m, scale, stream);
-    case 15: return launch<DT, 15>(in, in_stride, out, out_stride, m, scale, stream);
+    case 7: return launch<DT, 7>(in, in_stride, out, out_stride, m, sc, front, stream);
+    case 8: return launch<DT, 8>(in, in_stride, out, out_stride, m, sc, front, stream);
+    case 9: return launch<DT, 9>(in, in_stride, out, out_stride, m, sc, front, stream);
+    case 10: return launch<DT, 10>(in, in_stride, out, out_stride, m, sc, front, stream);
+    case 11: return launch<DT, 11>(in, in_stride, out, out_stride, m, sc, front, stream);
+    case 12: return launch<DT, 12>(in, in_stride, out, out_stride, m, sc, front, stream);
+    case 13: return launch<DT, 13>(in, in_stride, out, out_stride, m, sc, front, stream);
+    case 14: return launch<DT, 14>(in, in_stride, out, out_stride, m, sc, front, stream);
+    case 15: return launch<DT, 15>(in, in_stride, out, out_stride, m, sc, front, stream);
     default: return hipErrorInvalidValue;
   }
+}
+
+// HADACORE_VARIANT=valu|mfma forces a front end (testing and tuning); unset,
+// empty or anything else keeps the per-size table.  Read on every call.
+int front_override() {
+  const char *v = getenv("HADACORE_VARIANT");
+  if (v == nullptr) return -1;
+  if (strcmp(v, "valu") == 0) return kValu;
+  if (strcmp(v, "mfma") == 0) return kMfma;
+  return -1;
 }
 
 // Architecture check, cached per device: 0 unknown, 1 gfx950, 2 other.
@@ -516,10 +732,12 @@ extern "C" hadacore_status hadamard_transform_strided(const void *in, int64_t in
   const uint16_t *src = static_cast<const uint16_t *>(in);
   uint16_t *dst = static_cast<uint16_t *>(out);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  const ScaleArgs sc = split_scale(scale, dtype);
+  const int front = front_override();
   const hipError_t err =
       dtype == HADACORE_FP16
-          ? launch_dt<HADACORE_FP16>(L, src, in_row_stride, dst, out_row_stride, m, scale, s)
-          : launch_dt<HADACORE_BF16>(L, src, in_row_stride, dst, out_row_stride, m, scale, s);
+          ? launch_dt<HADACORE_FP16>(L, src, in_row_stride, dst, out_row_stride, m, sc, front, s)
+          : launch_dt<HADACORE_BF16>(L, src, in_row_stride, dst, out_row_stride, m, sc, front, s);
   return err == hipSuccess ? HADACORE_SUCCESS : HADACORE_ERROR_LAUNCH;
 }
 

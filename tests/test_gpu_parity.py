@@ -20,6 +20,9 @@ DTYPES = ["fp16", "bf16"]
 CODE = {"fp16": H.FP16, "bf16": H.BF16}
 
 
+VARIANTS = ["auto", "valu", "mfma"]
+
+
 @pytest.fixture(scope="module", autouse=True)
 def _device():
     import torch
@@ -27,6 +30,16 @@ def _device():
     H.library()  # fail loudly if the HIP library is missing
     yield
     torch.cuda.synchronize()
+
+
+@pytest.fixture(params=VARIANTS)
+def variant(request, monkeypatch):
+    """Front end of the transform: the per-size table ("auto") or forced VALU / matrix-core."""
+    if request.param == "auto":
+        monkeypatch.delenv("HADACORE_VARIANT", raising=False)
+    else:
+        monkeypatch.setenv("HADACORE_VARIANT", request.param)
+    return request.param
 
 
 def _run(bits: np.ndarray, dtype: str, scale: float, n: int, inplace: bool,
@@ -55,10 +68,10 @@ def _ragged_rows(L: int) -> int:
 @pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", range(7, 16))
-def test_every_size_ragged(oracle, L, dtype, inplace):
+def test_every_size_ragged(oracle, L, dtype, inplace, variant):
     n = 1 << L
     m = _ragged_rows(L)
-    say(f"every_size n={n} m={m} {dtype} inplace={inplace}")
+    say(f"every_size n={n} m={m} {dtype} inplace={inplace} variant={variant}")
     bits = W.random_rows(m, n, dtype, seed=1000 + L)
     s = W.default_scale(n)
     out = _run(bits, dtype, s, n, inplace)
@@ -94,7 +107,7 @@ def test_sweep_full_size_sampled(oracle, L, dtype):
 
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", [7, 8, 11, 12, 13, 15])
-def test_single_row(oracle, L, dtype):
+def test_single_row(oracle, L, dtype, variant):
     n = 1 << L
     bits = W.random_rows(1, n, dtype, seed=7 + L)
     out = _run(bits, dtype, 0.5, n, False)
@@ -113,7 +126,7 @@ def test_zero_rows_leaves_output_untouched():
 
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", [7, 9, 12, 14])
-def test_strided_rows_keep_gaps(oracle, L, dtype):
+def test_strided_rows_keep_gaps(oracle, L, dtype, variant):
     n = 1 << L
     m = 19
     in_stride, out_stride = n + 24, n + 40
@@ -152,7 +165,7 @@ def test_large_offsets(oracle, dtype):
 
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", [7, 10, 13, 15])
-def test_special_vectors(L, dtype):
+def test_special_vectors(L, dtype, variant):
     n = 1 << L
     one = W.round_to_bits(np.array([1.0], np.float32), dtype)[0]
     rows = np.zeros((4, n), np.uint16)
@@ -176,7 +189,7 @@ def test_special_vectors(L, dtype):
 
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", [7, 12, 15])
-def test_nonfinite_and_subnormal_inputs(oracle, L, dtype):
+def test_nonfinite_and_subnormal_inputs(oracle, L, dtype, variant):
     n = 1 << L
     bits = W.random_rows(6, n, dtype, seed=3)
     nan = 0x7E00 if dtype == "fp16" else 0x7FC0
@@ -196,7 +209,7 @@ def test_nonfinite_and_subnormal_inputs(oracle, L, dtype):
 
 
 @pytest.mark.parametrize("L", [7, 12, 15])
-def test_bf16_huge_values_do_not_overflow(oracle, L):
+def test_bf16_huge_values_do_not_overflow(oracle, L, variant):
     n = 1 << L
     rng = np.random.default_rng(L)
     vals = (rng.choice([-1.0, 1.0], (8, n)) * rng.uniform(1e36, 3e37, (8, n))).astype(np.float32)
@@ -210,7 +223,7 @@ def test_bf16_huge_values_do_not_overflow(oracle, L):
 
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", range(7, 16))
-def test_deterministic_and_inplace_equals_out_of_place(L, dtype):
+def test_deterministic_and_inplace_equals_out_of_place(L, dtype, variant):
     n = 1 << L
     m = 4096 >> max(0, L - 10) if L <= 12 else 9
     bits = W.random_rows(m, n, dtype, seed=L + 50)
