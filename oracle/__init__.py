@@ -10,7 +10,9 @@ What is computed (paper Sec. 2.1-2.2): for an m x n matrix of fp16/bf16 rows,
 ``y[i, j] = s * sum_k (-1)**popcount(j & k) * x[i, k]``, i.e. ``x @ H_n * s``
 with ``H_n`` the Sylvester-ordered Walsh-Hadamard matrix.  ``fwht`` follows the
 iterative radix-2 algorithm of Sec. 2.2; ``fwht_direct`` evaluates the plain
-definition one output at a time.
+definition one output at a time; ``fwht_fp8`` adds per-row FP8 (e4m3)
+quantization of the transformed rows (the fused transform + quantization the
+paper names as future work, Sec. 5).
 """
 from __future__ import annotations
 
@@ -77,6 +79,15 @@ class Oracle:
         lib.oracle_fwht_direct_f64.argtypes = [u16p, i64, i64, ctypes.c_int, ctypes.c_double,
                                                i64p, i64p, i64, f64p]
         lib.oracle_fwht_direct_f64.restype = ctypes.c_int
+        u8p = ctypes.POINTER(ctypes.c_uint8)
+        f32p = ctypes.POINTER(ctypes.c_float)
+        lib.oracle_decode_e4m3.argtypes = [ctypes.c_uint8]
+        lib.oracle_decode_e4m3.restype = ctypes.c_double
+        lib.oracle_encode_e4m3.argtypes = [ctypes.c_float]
+        lib.oracle_encode_e4m3.restype = ctypes.c_uint8
+        lib.oracle_fwht_fp8.argtypes = [u16p, i64, i64, i64, ctypes.c_int, ctypes.c_double, u8p,
+                                        i64, f32p]
+        lib.oracle_fwht_fp8.restype = ctypes.c_int
         self.lib = lib
 
     # -- decoders ---------------------------------------------------------
@@ -140,6 +151,41 @@ class Oracle:
         if rc:
             raise ValueError("oracle_fwht_direct_f64 rejected its arguments")
         return out
+
+    # -- fused transform + FP8 quantization ----------------------------------
+    def encode_e4m3(self, values) -> np.ndarray:
+        """OCP e4m3 codes (round-to-nearest-even) of float32 values."""
+        v = np.asarray(values, dtype=np.float32)
+        f = self.lib.oracle_encode_e4m3
+        return np.fromiter((f(float(x)) for x in v.ravel()), dtype=np.uint8,
+                           count=v.size).reshape(v.shape)
+
+    def decode_e4m3(self, codes) -> np.ndarray:
+        """Exact values of OCP e4m3 codes."""
+        c = np.asarray(codes, dtype=np.uint8)
+        table = np.array([self.lib.oracle_decode_e4m3(i) for i in range(256)], dtype=np.float64)
+        return table[c]
+
+    def fwht_fp8(self, bits: np.ndarray, dtype, scale: float, n: int | None = None):
+        """Fused transform + per-row e4m3 quantization: (codes (m, n) uint8, scales (m,) float32)."""
+        bits = np.ascontiguousarray(bits, dtype=np.uint16)
+        m, stride = bits.shape
+        n = stride if n is None else int(n)
+        codes = np.empty((m, n), dtype=np.uint8)
+        scales = np.empty(m, dtype=np.float32)
+        rc = self.lib.oracle_fwht_fp8(_u16(bits), stride, m, n, _dtype_code(dtype), float(scale),
+                                      _u8(codes), n, _f32(scales))
+        if rc:
+            raise ValueError("oracle_fwht_fp8 rejected its arguments")
+        return codes, scales
+
+
+def _u8(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8))
+
+
+def _f32(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
 
 
 def _u16(a):

@@ -15,7 +15,10 @@
  * The caller passes s; the paper's normalization (Sec. 2.2, the per-stage
  * division by sqrt 2 in its FWHT listing) is the special case s = 1/sqrt(n).
  *
- * Two independent routes are provided:
+ * Also: oracle_fwht_fp8, the transform followed by per-row FP8 (e4m3)
+ * quantization (see its comment), with its own e4m3 encoder and decoder.
+ *
+ * Two independent routes are provided for the transform itself:
  *   oracle_fwht_f64        -- the iterative radix-2 FWHT of Sec. 2.2: stage
  *                             sizes h = 1, 2, 4, ..., n/2; within a stage,
  *                             blocks of 2h, pairs (j, j+h) replaced by
@@ -213,5 +216,108 @@ int oracle_fwht_direct_f64(const uint16_t *in, int64_t in_stride, int64_t n, int
         }
         out[t] = acc * scale;
     }
+    return 0;
+}
+
+/* ---- fused transform + FP8 quantization -------------------------------------
+ *
+ * The paper names a fused Hadamard transform and quantization as future work
+ * (Sec. 5; the rotation exists to spread outliers before low-precision
+ * attention, Sec. 1 and Sec. 4.2).  Reading taken here: each transformed row
+ * y_i is quantized to OCP FP8 e4m3 (finite max 448, no infinities) with one
+ * fp32 scale per row,
+ *     amax_i = max_j |y_ij|   (NaN entries ignored unless all are NaN)
+ *     s_i    = amax_i / 448
+ *     q_ij   = e4m3_rne(y_ij * inv_i),  inv_i = 448 / amax_i if amax_i > 0 else 0
+ * so that y_ij ~ decode(q_ij) * s_i.  The quantization decision is taken in
+ * fp32, as the GPU kernel takes it: y is the fp64 transform rounded once to
+ * fp32, and s, inv and the product are fp32 operations.
+ */
+
+/* e4m3 (OCP "fn" variant): 1 sign, 4 exponent bits (bias 7), 3 fraction bits;
+ * exponent field 15 with fraction 7 is NaN; there is no infinity. */
+double oracle_decode_e4m3(uint8_t q)
+{
+    int sign = (q >> 7) & 1;
+    int expo = (q >> 3) & 0xf;
+    int frac = q & 0x7;
+    double v;
+    if (expo == 15 && frac == 7) return NAN;
+    if (expo == 0)
+        v = ldexp((double)frac, -9);               /* subnormal: frac * 2^-9 */
+    else
+        v = ldexp((double)(8 + frac), expo - 10);  /* (1.f) * 2^(e-7) */
+    return sign ? -v : v;
+}
+
+/* Round-to-nearest-even of a float to e4m3.  464 is the tie between 448 and
+ * the missing 480 and rounds to the even 448; larger magnitudes and NaN give
+ * NaN (0x7f with the sign). */
+uint8_t oracle_encode_e4m3(float x)
+{
+    uint8_t sign = signbit(x) ? 0x80 : 0x00;
+    double a = fabs((double)x);
+    if (isnan(x) || a > 464.0) return (uint8_t)(sign | 0x7f);
+    /* candidates are k * 2^(e-3) in the binade [2^e, 2^(e+1)), e >= -6;
+     * below 2^-6 the spacing is 2^-9 (subnormals) */
+    int e;
+    double spacing;
+    if (a < ldexp(1.0, -6)) {
+        spacing = ldexp(1.0, -9);
+    } else {
+        frexp(a, &e);          /* a = f * 2^e, f in [0.5, 1) */
+        spacing = ldexp(1.0, e - 1 - 3);
+    }
+    double k = a / spacing;            /* exact: spacing is a power of two */
+    double kf = floor(k);
+    double r = k - kf;
+    if (r > 0.5 || (r == 0.5 && fmod(kf, 2.0) != 0.0)) kf += 1.0;
+    double v = kf * spacing;           /* rounded magnitude, <= 448 */
+    /* encode v */
+    if (v == 0.0) return sign;
+    if (v < ldexp(1.0, -6)) return (uint8_t)(sign | (uint8_t)(v / ldexp(1.0, -9)));
+    frexp(v, &e);                      /* v = f * 2^e, 2^(e-1) <= v < 2^e */
+    int biased = (e - 1) + 7;
+    int frac = (int)(v / ldexp(1.0, e - 1 - 3)) - 8;
+    return (uint8_t)(sign | (biased << 3) | frac);
+}
+
+/* fp32 maximum that ignores NaN unless both operands are NaN. */
+static float max_ignoring_nan(float a, float b)
+{
+    if (isnan(a)) return b;
+    if (isnan(b)) return a;
+    return a > b ? a : b;
+}
+
+/*
+ * Fused transform + quantization of m rows: codes (m x n bytes, row stride
+ * out_stride) and scales (m floats).  Returns 0 on success, 1 on bad
+ * arguments.
+ */
+int oracle_fwht_fp8(const uint16_t *in, int64_t in_stride, int64_t m, int64_t n, int dtype,
+                    double scale, uint8_t *codes, int64_t out_stride, float *scales)
+{
+    if (m < 0 || !is_pow2(n) || in_stride < n || out_stride < n) return 1;
+    if (dtype != ORACLE_FP16 && dtype != ORACLE_BF16) return 1;
+    double *row = (double *)malloc((size_t)n * sizeof(double));
+    float *y = (float *)malloc((size_t)n * sizeof(float));
+    if (!row || !y) { free(row); free(y); return 1; }
+    for (int64_t i = 0; i < m; ++i) {
+        const uint16_t *src = in + i * in_stride;
+        for (int64_t k = 0; k < n; ++k) row[k] = decode(src[k], dtype);
+        oracle_fwht_vec_f64(row, n);
+        float amax = NAN;
+        for (int64_t k = 0; k < n; ++k) {
+            y[k] = (float)(row[k] * scale);
+            amax = max_ignoring_nan(amax, fabsf(y[k]));
+        }
+        const float s = amax / 448.0f;
+        const float inv = amax > 0.0f ? 448.0f / amax : 0.0f;
+        scales[i] = s;
+        for (int64_t k = 0; k < n; ++k) codes[i * out_stride + k] = oracle_encode_e4m3(y[k] * inv);
+    }
+    free(row);
+    free(y);
     return 0;
 }

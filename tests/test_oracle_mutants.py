@@ -2,7 +2,8 @@
 
 Each case copies ``oracle/fwht_oracle.c``, plants one mistake (a flipped
 butterfly sign, a dropped stage, a wrong pair index, an off-by-one exponent
-bias, a missing scale, an ignored stride ...), compiles the copy on the CPU
+bias, a missing scale, an ignored stride, a wrong FP8 rounding rule or scale
+constant ...), compiles the copy on the CPU
 into a temporary library and runs the pin battery of ``test_oracle.py``
 against it.  At least one pin must fail for every mutant.  The real oracle
 source is never modified.
@@ -14,6 +15,7 @@ import pytest
 
 import oracle as oracle_pkg
 import test_oracle as T
+import test_oracle_fp8 as F
 
 MUTANTS = [
     ("butterfly_sign", "v[j + h] = a - b;", "v[j + h] = b - a;"),
@@ -34,6 +36,17 @@ MUTANTS = [
     ("direct_scale_missing", "out[t] = acc * scale;", "out[t] = acc;"),
     ("thread_remainder_rows_dropped", "jobs[t].row1 = m * (t + 1) / nthreads;",
      "jobs[t].row1 = m * t / nthreads + m / nthreads;"),
+    # fused FP8 quantization
+    ("e4m3_ties_away", "if (r > 0.5 || (r == 0.5 && fmod(kf, 2.0) != 0.0)) kf += 1.0;",
+     "if (r >= 0.5) kf += 1.0;"),
+    ("e4m3_exponent_bias", "int biased = (e - 1) + 7;", "int biased = (e - 1) + 8;"),
+    ("e4m3_overflow_threshold", "a > 464.0", "a > 448.0"),
+    ("e4m3_subnormal_spacing", "spacing = ldexp(1.0, -9);", "spacing = ldexp(1.0, -10);"),
+    ("e4m3_decode_bias", "expo - 10", "expo - 11"),
+    ("fp8_scale_constant", "const float s = amax / 448.0f;", "const float s = amax / 480.0f;"),
+    ("fp8_zero_guard", "amax > 0.0f ? 448.0f / amax : 0.0f", "448.0f / amax"),
+    ("fp8_amax_without_abs", "amax = max_ignoring_nan(amax, fabsf(y[k]));",
+     "amax = max_ignoring_nan(amax, y[k]);"),
 ]
 
 
@@ -53,6 +66,11 @@ def _pins(o):
         lambda: T.test_strided_rows_ignore_gaps(o),
         lambda: T.test_scale_is_one_final_product(o),
         lambda: T.test_threads_do_not_change_results(o),
+        lambda: F.test_decode_e4m3_every_code(o),
+        lambda: F.test_encode_e4m3_matches_torch(o),
+        lambda: F.test_hand_derived_fixtures(o),
+        lambda: F.test_quantization_properties(o, "bf16", 10),
+        lambda: F.test_special_rows(o),
     ]
 
 
