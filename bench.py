@@ -45,6 +45,8 @@ def parse_args(argv=None):
     p.add_argument("--workload", default="bf16_1048576x128_inplace",
                    help="a named workload (workloads.WORKLOADS) or sweep:<dtype>:<log2 n>:<in|out>")
     p.add_argument("--sweep", metavar="FILE", help="also time every workload, one JSON line each")
+    p.add_argument("--fp8", action="store_true",
+                   help="time the fused transform + e4m3 quantization instead of the transform")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="target duration of the CPU oracle baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -124,42 +126,56 @@ class Device:
         return start.elapsed_time(end) / 1e3
 
 
-def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0) -> dict:
+def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0,
+                  fp8: bool = False) -> dict:
+    """Time one workload: the transform (16-bit out, in place or not) or, with fp8,
+    the fused transform + per-row e4m3 quantization (codes + scales out)."""
     from paper_2412_08832_amd import workloads as W
     H, torch = d.H, d.torch
     bits = W.generate(w)
     code = H.FP16 if w.dtype == "fp16" else H.BF16
     nbytes = w.m * w.n * 2
-    per_set = nbytes if w.inplace else 2 * nbytes
+    per_set = nbytes + (w.m * w.n + 4 * w.m if fp8 else (0 if w.inplace else nbytes))
     nbuf = max(2, math.ceil(ROTATING_BYTES / per_set))
     first = d.upload(bits, w.dtype)
     del bits
     ins = [first] + [first.clone() for _ in range(nbuf - 1)]
-    outs = ins if w.inplace else [torch.empty_like(first) for _ in range(nbuf)]
     s = d.stream.cuda_stream
-    calls = [
-        (lambda i=i: H.hadamard_transform(ins[i].data_ptr(), outs[i].data_ptr(), w.m, w.n, code,
-                                          w.scale, s))
-        for i in range(nbuf)
-    ]
+    if fp8:
+        codes = [torch.empty((w.m, w.n), dtype=torch.uint8, device=d.dev) for _ in range(nbuf)]
+        scales = [torch.empty((w.m,), dtype=torch.float32, device=d.dev) for _ in range(nbuf)]
+        calls = [
+            (lambda i=i: H.hadamard_transform_fp8(ins[i].data_ptr(), w.n, codes[i].data_ptr(), w.n,
+                                                  scales[i].data_ptr(), w.m, w.n, code, w.scale, s))
+            for i in range(nbuf)
+        ]
+        alg_bytes = w.m * w.n * 3 + 4 * w.m          # 16-bit read, e4m3 write, one scale per row
+        outs = codes
+    else:
+        outs = ins if w.inplace else [torch.empty_like(first) for _ in range(nbuf)]
+        calls = [
+            (lambda i=i: H.hadamard_transform(ins[i].data_ptr(), outs[i].data_ptr(), w.m, w.n, code,
+                                              w.scale, s))
+            for i in range(nbuf)
+        ]
+        alg_bytes = 2 * nbytes                      # one read + one write of every element
     sec = d.time_calls(calls, steps, warmup, min_warm_s)
     per_launch = sec / steps
-    alg_bytes = 2 * nbytes                      # one read + one write of every element
     gbs = alg_bytes / per_launch / 1e9
 
-    # device copy of the same bytes: the achievable-bandwidth reference
-    srcs = ins
-    dsts = [torch.empty_like(first) for _ in range(nbuf)] if w.inplace else outs
+    # device copy of the same element bytes: the achievable-bandwidth reference
+    dsts = [torch.empty_like(first) for _ in range(nbuf)] if (w.inplace or fp8) else outs
     copies = [
-        (lambda i=i: H.hadacore_stream_copy(srcs[i].data_ptr(), dsts[i].data_ptr(), nbytes, s))
+        (lambda i=i: H.hadacore_stream_copy(ins[i].data_ptr(), dsts[i].data_ptr(), nbytes, s))
         for i in range(nbuf)
     ]
     csec = d.time_calls(copies, steps, warmup, min_warm_s) / steps
-    copy_gbs = alg_bytes / csec / 1e9
-    del ins, outs, srcs, dsts, first
+    copy_gbs = 2 * nbytes / csec / 1e9
+    del ins, outs, dsts, first, calls
     torch.cuda.empty_cache()
     return {
-        "workload": w.name, "dtype": w.dtype, "m": w.m, "n": w.n, "inplace": w.inplace,
+        "workload": w.name + ("_fp8" if fp8 else ""), "dtype": w.dtype, "m": w.m, "n": w.n,
+        "inplace": w.inplace and not fp8, "fp8": fp8,
         "steps": steps, "rotating_buffers": nbuf, "ms_per_step": per_launch * 1e3,
         "elements_per_s": w.m * w.n / per_launch, "gbs": gbs, "frac_hbm_peak": gbs / HBM_PEAK_GBS,
         "copy_gbs": copy_gbs, "frac_of_copy": gbs / copy_gbs, "alg_bytes_per_launch": alg_bytes,
@@ -217,9 +233,9 @@ def main(argv=None) -> int:
         return 2
     w = workload_by_name(args.workload)
     d = Device()
-    r = time_workload(d, w, args.steps, args.warmup)
+    r = time_workload(d, w, args.steps, args.warmup, fp8=args.fp8)
     digest = source_digest()
-    traffic = measured_traffic(w.name, digest)
+    traffic = measured_traffic(r["workload"], digest)
     line = {
         "metric": METRIC,
         "value": r["elements_per_s"],
@@ -234,7 +250,8 @@ def main(argv=None) -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": w.name, "m": w.m, "n": w.n, "io_dtype": w.dtype, "inplace": w.inplace,
+            "workload": r["workload"], "m": w.m, "n": w.n, "io_dtype": w.dtype,
+            "inplace": r["inplace"], "output": "e4m3 codes + fp32 row scales" if args.fp8 else w.dtype,
             "scale": w.scale, "rotating_buffers": r["rotating_buffers"],
             "achieved_gbs": r["gbs"], "frac_hbm_peak": r["frac_hbm_peak"],
             "copy_gbs": r["copy_gbs"], "frac_of_copy": r["frac_of_copy"],
@@ -250,12 +267,15 @@ def main(argv=None) -> int:
         for inplace in (True, False):
             for dt in ("fp16", "bf16"):
                 points += [W.sweep_point(k, dt, inplace) for k in range(7, 16)]
+        fp8_points = [W.sweep_point(k, "bf16", False) for k in range(7, 16)]
+        fp8_points += [W.WORKLOADS["bf16_1048576x128_inplace"], W.WORKLOADS["fp16_16384x4096"]]
+        jobs = [(p, False) for p in points] + [(p, True) for p in fp8_points]
         with open(args.sweep, "w") as f:
-            for p in points:
-                pr = time_workload(d, p, args.steps, args.warmup, min_warm_s=0.03)
+            for p, fp8 in jobs:
+                pr = time_workload(d, p, args.steps, args.warmup, min_warm_s=0.03, fp8=fp8)
                 f.write(json.dumps(pr) + "\n")
                 f.flush()
-                print(f"[sweep] {p.name}: {pr['gbs']:.0f} GB/s ({100 * pr['frac_hbm_peak']:.1f}% "
+                print(f"[sweep] {pr['workload']}: {pr['gbs']:.0f} GB/s ({100 * pr['frac_hbm_peak']:.1f}% "
                       f"of peak, {100 * pr['frac_of_copy']:.1f}% of copy)", file=sys.stderr,
                       flush=True)
     if not args.no_cpu_baseline:

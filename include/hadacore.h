@@ -98,6 +98,29 @@ hadacore_status hadamard_transform_strided(const void *in, int64_t in_row_stride
                                            hadacore_dtype dtype, float scale, void *stream);
 
 /*
+ * hadamard_transform_fp8 -- the transform fused with per-row quantization to
+ * OCP FP8 e4m3 (the fused Hadamard transform + quantization that the paper
+ * names as future work, Sec. 5; rotations precede FP8 attention, Sec. 4.2).
+ * For every row i, with y = scale * in[i] * H_n computed as above:
+ *     amax_i          = max_j |y_j|   (NaN ignored unless the row is all NaN)
+ *     out_scales[i]   = amax_i / 448  (fp32, correctly rounded)
+ *     out_codes[i][j] = e4m3 round-to-nearest-even of y_j * (448 / amax_i)
+ *                       (448/amax_i taken as 0 when amax_i is 0)
+ * so that y_j ~ decode_e4m3(out_codes[i][j]) * out_scales[i].  e4m3: 1 sign,
+ * 4 exponent (bias 7) and 3 fraction bits, largest finite 448, 0x7f NaN.
+ *   in              device pointer, m rows of n 16-bit values at in_row_stride
+ *                   elements (>= n, multiple of 8), 16-byte aligned
+ *   out_codes       device pointer, m rows of n bytes at out_row_stride bytes
+ *                   (>= n, multiple of 16), 16-byte aligned
+ *   out_scales      device pointer to m floats, 4-byte aligned
+ * The three ranges must not overlap (OVERLAP otherwise).  Other arguments,
+ * streams, ownership and errors as for hadamard_transform.
+ */
+hadacore_status hadamard_transform_fp8(const void *in, int64_t in_row_stride, void *out_codes,
+                                       int64_t out_row_stride, float *out_scales, int64_t m,
+                                       int64_t n, hadacore_dtype dtype, float scale, void *stream);
+
+/*
  * hadacore_stream_copy -- copies `bytes` bytes from device pointer `src` to
  * device pointer `dst` with 16-byte vector loads and stores on `stream`.  Both
  * pointers 16-byte aligned, bytes a multiple of 16, ranges disjoint.  It moves

@@ -396,6 +396,107 @@ struct ScaleArgs {
   int e2;
 };
 
+// ---- fused FP8 epilogue ------------------------------------------------------------
+//
+// The transform followed by per-row quantization to OCP FP8 e4m3 (the fused
+// transform + quantization the paper names as future work, Sec. 5):
+//   amax = max_j |y_j| (NaN ignored unless the row is all NaN), s = amax/448,
+//   code_j = e4m3_rne(y_j * inv) with inv = 448/amax (0 for a zero row),
+// the divisions correctly rounded in fp32.  y ~ decode(code) * s.
+
+constexpr int kStore16 = 0;  // 16-bit output in the input dtype
+constexpr int kFp8 = 1;      // e4m3 codes + one fp32 scale per row
+
+struct Fp8Out {
+  uint8_t *codes;
+  int64_t stride;  // bytes between rows of codes
+  float *scales;   // one per row
+};
+
+typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+
+// Value of `x` held by lane (lane ^ (1 << LB)).
+template <int LB>
+__device__ __forceinline__ float lane_partner(float x, int lane) {
+  const int xi = __builtin_bit_cast(int, x);
+  int r;
+  if constexpr (LB == 0) {
+    r = __builtin_amdgcn_mov_dpp(xi, 0xB1, 0xF, 0xF, true);   // quad_perm:[1,0,3,2]
+  } else if constexpr (LB == 1) {
+    r = __builtin_amdgcn_mov_dpp(xi, 0x4E, 0xF, 0xF, true);   // quad_perm:[2,3,0,1]
+  } else if constexpr (LB == 2) {
+    r = __builtin_amdgcn_ds_swizzle(xi, 0x101F);              // xor 4
+  } else if constexpr (LB == 3) {
+    r = __builtin_amdgcn_mov_dpp(xi, 0x128, 0xF, 0xF, true);  // row_ror:8 == xor 8
+  } else if constexpr (LB == 4) {
+    r = __builtin_amdgcn_ds_swizzle(xi, 0x401F);              // xor 16
+  } else {
+    r = __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, xi);   // xor 32
+  }
+  return __builtin_bit_cast(float, r);
+}
+
+// Maximum over the lanes that differ from this one only in the lane bits of MASK.
+template <int MASK>
+__device__ __forceinline__ float lane_max(float x, int lane) {
+  if constexpr ((MASK & 1) != 0) x = fmaxf(x, lane_partner<0>(x, lane));
+  if constexpr ((MASK & 2) != 0) x = fmaxf(x, lane_partner<1>(x, lane));
+  if constexpr ((MASK & 4) != 0) x = fmaxf(x, lane_partner<2>(x, lane));
+  if constexpr ((MASK & 8) != 0) x = fmaxf(x, lane_partner<3>(x, lane));
+  if constexpr ((MASK & 16) != 0) x = fmaxf(x, lane_partner<4>(x, lane));
+  if constexpr ((MASK & 32) != 0) x = fmaxf(x, lane_partner<5>(x, lane));
+  return x;
+}
+
+// Lane bits along which one row's elements are spread after the stages.
+template <int FRONT, int L>
+constexpr int row_lane_mask() {
+  return FRONT == kValu ? lane_stage_mask<kValu, L>() : (lane_stage_mask<kMfma, L>() | 0x30);
+}
+
+__device__ __forceinline__ float abs_max8(const float *v) {
+  float a = fabsf(v[0]);
+#pragma unroll
+  for (int j = 1; j < 8; ++j) a = fmaxf(a, fabsf(v[j]));
+  return a;
+}
+
+// 8 values times `mul` to 8 e4m3 codes, round-to-nearest-even (v_cvt_pk_fp8_f32).
+__device__ __forceinline__ u2 to_e4m3x8(const float *v, float mul) {
+  int lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[0] * mul, v[1] * mul, 0, false);
+  lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[2] * mul, v[3] * mul, lo, true);
+  int hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[4] * mul, v[5] * mul, 0, false);
+  hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[6] * mul, v[7] * mul, hi, true);
+  return u2{(uint32_t)lo, (uint32_t)hi};
+}
+
+template <bool NT>
+__device__ __forceinline__ void gstore8(uint8_t *p, u2 v) {
+  u2 *q = reinterpret_cast<u2 *>(p);
+  if constexpr (NT) {
+    __builtin_nontemporal_store(v, q);
+  } else {
+    *q = v;
+  }
+}
+
+// Quantization multiplier of a lane: the twist sign (and, for kMfma, the part
+// of the scale the front end left out) times 448/amax; amax is the row's
+// largest |y| given the largest |register| of the row.
+template <int FRONT>
+struct Fp8Quant {
+  float amax;
+  float mul;
+  __device__ __forceinline__ Fp8Quant(float reg_amax, bool tw, float post) {
+    const float mag = FRONT == kMfma ? fabsf(post) : 1.0f;
+    amax = reg_amax * mag;
+    const float inv = amax > 0.0f ? 448.0f / amax : 0.0f;
+    // true value = register * (twist sign) * (kMfma: post), quantized as true * inv
+    const float to_true = FRONT == kMfma ? (tw ? -post : post) : (tw ? -1.0f : 1.0f);
+    mul = to_true * inv;
+  }
+};
+
 // ---- kernels ------------------------------------------------------------------
 
 // n <= 512*C: a tile of 512*C elements is 512*C/n whole rows and every stage
@@ -404,10 +505,10 @@ struct ScaleArgs {
 // constants, signs, addressing) is paid once per T tiles while only one or two
 // tiles per wave are in flight.  WPB independent waves per workgroup.  Only
 // the last tile can end past row m; it masks those rows.
-template <int DT, int L, int C, int T, int WPB, bool NT, int FRONT>
+template <int DT, int L, int C, int T, int WPB, bool NT, int FRONT, int EPI>
 __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
     const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, int64_t m,
-    ScaleArgs sc) {
+    ScaleArgs sc, Fp8Out fp8) {
   constexpr int kTile = 512 * C;
   static_assert((1 << L) <= kTile, "row does not fit a wave tile");
   constexpr int kRows = kTile >> L;
@@ -459,12 +560,48 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
     }
     wave_stages<FRONT, L, C>(v, lane);
     const bool full = row0 + kRows <= m;
-    uint16_t *dst = out + row0 * out_stride;
+    if constexpr (EPI == kStore16) {
+      uint16_t *dst = out + row0 * out_stride;
 #pragma unroll
-    for (int k = 0; k < C; ++k) {
-      const int t = (k * kWave + lf) * 8;
-      if (full || row0 + (t >> L) < m) {
-        gstore<NT>(dst + (int64_t)(t >> L) * out_stride + (t & kMask), fin(&v[k * 8]));
+      for (int k = 0; k < C; ++k) {
+        const int t = (k * kWave + lf) * 8;
+        if (full || row0 + (t >> L) < m) {
+          gstore<NT>(dst + (int64_t)(t >> L) * out_stride + (t & kMask), fin(&v[k * 8]));
+        }
+      }
+    } else {
+      // row maxima: within each chunk, across the chunks of one row, across its lanes
+      float a[C];
+#pragma unroll
+      for (int k = 0; k < C; ++k) a[k] = abs_max8(&v[k * 8]);
+      constexpr int kChunkRow = (C >= 2 && L > 9 ? 1 : 0) | (C >= 4 && L > 10 ? 2 : 0) |
+                                (C >= 8 && L > 11 ? 4 : 0);
+#pragma unroll
+      for (int bit = 1; bit < C; bit <<= 1) {
+        if ((kChunkRow & bit) != 0) {
+#pragma unroll
+          for (int k = 0; k < C; ++k) {
+            if ((k & bit) == 0) {
+              const float x = fmaxf(a[k], a[k | bit]);
+              a[k] = x;
+              a[k | bit] = x;
+            }
+          }
+        }
+      }
+      const bool tw = twisted<FRONT, L>(lane);
+      uint8_t *dst = fp8.codes + row0 * fp8.stride;
+#pragma unroll
+      for (int k = 0; k < C; ++k) {
+        const int t = (k * kWave + lf) * 8;
+        const Fp8Quant<FRONT> qz(lane_max<row_lane_mask<FRONT, L>()>(a[k], lane), tw, sc.post);
+        if (full || row0 + (t >> L) < m) {
+          gstore8<NT>(dst + (int64_t)(t >> L) * fp8.stride + (t & kMask),
+                      to_e4m3x8(&v[k * 8], qz.mul));
+          if ((lane & row_lane_mask<FRONT, L>()) == 0 && (k & kChunkRow) == 0) {
+            fp8.scales[row0 + (t >> L)] = qz.amax / 448.0f;
+          }
+        }
       }
     }
     if (!more) break;
@@ -479,9 +616,10 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
 // halves the LDS footprint (more workgroups per CU) at the cost of two extra
 // barriers.  The exchange keeps every value in its lane, so the lane layout
 // of the front end carries through to the store.
-template <int DT, int L, int C, int HALVES, bool NT, int FRONT>
+template <int DT, int L, int C, int HALVES, bool NT, int FRONT, int EPI>
 __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
-    const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc) {
+    const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc,
+    Fp8Out fp8) {
   constexpr int n = 1 << L;
   constexpr int NW = n / (512 * C);
   static_assert(NW >= 2 && NW <= C, "wave bits must fit the chunk bits");
@@ -495,7 +633,7 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   const int w = threadIdx.x / kWave;
   const int64_t row = blockIdx.x;
   const uint16_t *src = in + row * in_stride;
-  uint16_t *dst = out + row * out_stride;
+  uint16_t *dst = EPI == kStore16 ? out + row * out_stride : nullptr;
 
   u4 raw[C];
   const int lf_load = lane_field_load<FRONT, L>(lane);
@@ -537,12 +675,34 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   reg_stage<3>(v);
   if constexpr (NW >= 4) reg_stage<4>(v);
   if constexpr (NW >= 8) reg_stage<5>(v);
-  const Finisher<DT, FRONT> fin(twisted<FRONT, L>(lane), sc.post);
   const int lf = lane_field<FRONT, L>(lane);
+  if constexpr (EPI == kStore16) {
+    const Finisher<DT, FRONT> fin(twisted<FRONT, L>(lane), sc.post);
 #pragma unroll
-  for (int k = 0; k < C; ++k) {
-    const int W = (k % NW) * C + (k / NW) * NW + w;
-    gstore<NT>(dst + (W * kWave + lf) * 8, fin(&v[k * 8]));
+    for (int k = 0; k < C; ++k) {
+      const int W = (k % NW) * C + (k / NW) * NW + w;
+      gstore<NT>(dst + (W * kWave + lf) * 8, fin(&v[k * 8]));
+    }
+  } else {
+    // the row spans the workgroup: registers, then lanes, then waves (through LDS)
+    __shared__ float wave_max[NW];
+    float a = abs_max8(&v[0]);
+#pragma unroll
+    for (int k = 1; k < C; ++k) a = fmaxf(a, abs_max8(&v[k * 8]));
+    a = lane_max<0x3F>(a, lane);
+    if (lane == 0) wave_max[w] = a;
+    __syncthreads();
+    a = wave_max[0];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) a = fmaxf(a, wave_max[i]);
+    const Fp8Quant<FRONT> qz(a, twisted<FRONT, L>(lane), sc.post);
+    uint8_t *codes = fp8.codes + row * fp8.stride;
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      const int W = (k % NW) * C + (k / NW) * NW + w;
+      gstore8<NT>(codes + (W * kWave + lf) * 8, to_e4m3x8(&v[k * 8], qz.mul));
+    }
+    if (threadIdx.x == 0) fp8.scales[row] = qz.amax / 448.0f;
   }
 }
 
@@ -575,18 +735,20 @@ ScaleArgs split_scale(float scale, int dtype) {
 
 // C: chunks per lane; T: tiles per wave (wave kernel) ; WPB: waves per workgroup
 // (wave kernel); HALVES: LDS exchange passes (block kernel); FRONT: kValu / kMfma.
-template <int DT, int L, int C, int T, int WPB, int HALVES, int FRONT>
+template <int DT, int L, int C, int T, int WPB, int HALVES, int FRONT, int EPI = kStore16>
 hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
-                      int64_t m, const ScaleArgs &sc, hipStream_t stream) {
+                      int64_t m, const ScaleArgs &sc, hipStream_t stream, Fp8Out fp8 = {}) {
   if constexpr ((1 << L) <= 512 * C) {
     constexpr int64_t rows_per_wave = (int64_t)T * ((512 * C) >> L);
     const int64_t waves = (m + rows_per_wave - 1) / rows_per_wave;
     const int64_t blocks = (waves + WPB - 1) / WPB;
-    hipLaunchKernelGGL((fwht_wave_kernel<DT, L, C, T, WPB, true, FRONT>), dim3((uint32_t)blocks),
-                       dim3(kWave * WPB), 0, stream, in, in_stride, out, out_stride, m, sc);
+    hipLaunchKernelGGL((fwht_wave_kernel<DT, L, C, T, WPB, true, FRONT, EPI>),
+                       dim3((uint32_t)blocks), dim3(kWave * WPB), 0, stream, in, in_stride, out,
+                       out_stride, m, sc, fp8);
   } else {
-    hipLaunchKernelGGL((fwht_block_kernel<DT, L, C, HALVES, true, FRONT>), dim3((uint32_t)m),
-                       dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out, out_stride, sc);
+    hipLaunchKernelGGL((fwht_block_kernel<DT, L, C, HALVES, true, FRONT, EPI>), dim3((uint32_t)m),
+                       dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out, out_stride, sc,
+                       fp8);
   }
   return hipGetLastError();
 }
@@ -599,15 +761,17 @@ hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int6
 // waves with one LDS exchange.  The matrix-core front end wins from n = 2048
 // on (except 16384); below that the VALU front is as fast and simpler.
 // `front` < 0 takes the table's choice; kValu / kMfma force one front end.
-template <int DT, int L>
+template <int DT, int L, int EPI>
 hipError_t launch(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
-                  int64_t m, const ScaleArgs &sc, int front, hipStream_t stream) {
+                  int64_t m, const ScaleArgs &sc, int front, hipStream_t stream, Fp8Out fp8) {
   //                             default front       C  T  WPB HALVES
   constexpr int kDefault = (L >= 11 && L != 14) ? kMfma : kValu;
   const bool mfma = front < 0 ? kDefault == kMfma : front == kMfma;
 #define HC_CFG(C, T, WPB, H)                                                                     \
-  (mfma ? launch_cfg<DT, L, C, T, WPB, H, kMfma>(in, in_stride, out, out_stride, m, sc, stream)  \
-        : launch_cfg<DT, L, C, T, WPB, H, kValu>(in, in_stride, out, out_stride, m, sc, stream))
+  (mfma ? launch_cfg<DT, L, C, T, WPB, H, kMfma, EPI>(in, in_stride, out, out_stride, m, sc,      \
+                                                     stream, fp8)                                 \
+        : launch_cfg<DT, L, C, T, WPB, H, kValu, EPI>(in, in_stride, out, out_stride, m, sc,      \
+                                                     stream, fp8))
   if constexpr (L <= 9) {
     return HC_CFG(1, 1, 1, 1);
   } else if constexpr (L == 10) {
@@ -617,28 +781,30 @@ hipError_t launch(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t 
   } else if constexpr (L == 12) {
     return HC_CFG(4, 1, 1, 1);
   } else if constexpr (L == 13) {
-    return mfma ? launch_cfg<DT, L, 4, 1, 1, 1, kMfma>(in, in_stride, out, out_stride, m, sc, stream)
-                : launch_cfg<DT, L, 4, 1, 1, 2, kValu>(in, in_stride, out, out_stride, m, sc, stream);
+    return mfma ? launch_cfg<DT, L, 4, 1, 1, 1, kMfma, EPI>(in, in_stride, out, out_stride, m, sc,
+                                                           stream, fp8)
+                : launch_cfg<DT, L, 4, 1, 1, 2, kValu, EPI>(in, in_stride, out, out_stride, m, sc,
+                                                           stream, fp8);
   } else {
     return HC_CFG(8, 1, 1, 2);
   }
 #undef HC_CFG
 }
 
-template <int DT>
+template <int DT, int EPI = kStore16>
 hipError_t launch_dt(int L, const uint16_t *in, int64_t in_stride, uint16_t *out,
                      int64_t out_stride, int64_t m, const ScaleArgs &sc, int front,
-                     hipStream_t stream) {
+                     hipStream_t stream, Fp8Out fp8 = {}) {
   switch (L) {
-    case 7: return launch<DT, 7>(in, in_stride, out, out_stride, m, sc, front, stream);
-    case 8: return launch<DT, 8>(in, in_stride, out, out_stride, m, sc, front, stream);
-    case 9: return launch<DT, 9>(in, in_stride, out, out_stride, m, sc, front, stream);
-    case 10: return launch<DT, 10>(in, in_stride, out, out_stride, m, sc, front, stream);
-    case 11: return launch<DT, 11>(in, in_stride, out, out_stride, m, sc, front, stream);
-    case 12: return launch<DT, 12>(in, in_stride, out, out_stride, m, sc, front, stream);
-    case 13: return launch<DT, 13>(in, in_stride, out, out_stride, m, sc, front, stream);
-    case 14: return launch<DT, 14>(in, in_stride, out, out_stride, m, sc, front, stream);
-    case 15: return launch<DT, 15>(in, in_stride, out, out_stride, m, sc, front, stream);
+    case 7: return launch<DT, 7, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
+    case 8: return launch<DT, 8, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
+    case 9: return launch<DT, 9, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
+    case 10: return launch<DT, 10, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
+    case 11: return launch<DT, 11, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
+    case 12: return launch<DT, 12, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
+    case 13: return launch<DT, 13, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
+    case 14: return launch<DT, 14, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
+    case 15: return launch<DT, 15, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
     default: return hipErrorInvalidValue;
   }
 }
@@ -744,6 +910,52 @@ extern "C" hadacore_status hadamard_transform_strided(const void *in, int64_t in
 extern "C" hadacore_status hadamard_transform(const void *in, void *out, int64_t m, int64_t n,
                                               hadacore_dtype dtype, float scale, void *stream) {
   return hadamard_transform_strided(in, n, out, n, m, n, dtype, scale, stream);
+}
+
+extern "C" hadacore_status hadamard_transform_fp8(const void *in, int64_t in_row_stride,
+                                                  void *out_codes, int64_t out_row_stride,
+                                                  float *out_scales, int64_t m, int64_t n,
+                                                  hadacore_dtype dtype, float scale, void *stream) {
+  if (m < 0) return HADACORE_ERROR_INVALID_VALUE;
+  const int L = log2_exact(n);
+  if (L < 7 || L > 15) return HADACORE_ERROR_INVALID_SIZE;
+  if (dtype != HADACORE_FP16 && dtype != HADACORE_BF16) return HADACORE_ERROR_INVALID_DTYPE;
+  if (!isfinite(scale)) return HADACORE_ERROR_INVALID_VALUE;
+  if (in_row_stride < n || (in_row_stride % 8) != 0 || out_row_stride < n ||
+      (out_row_stride % 16) != 0)
+    return HADACORE_ERROR_INVALID_STRIDE;
+  if (m == 0) return HADACORE_SUCCESS;
+  if (in == nullptr || out_codes == nullptr || out_scales == nullptr)
+    return HADACORE_ERROR_INVALID_VALUE;
+  if ((reinterpret_cast<uintptr_t>(in) & 15) != 0 ||
+      (reinterpret_cast<uintptr_t>(out_codes) & 15) != 0 ||
+      (reinterpret_cast<uintptr_t>(out_scales) & 3) != 0)
+    return HADACORE_ERROR_MISALIGNED;
+  if (m >= (int64_t(1) << 31)) return HADACORE_ERROR_TOO_LARGE;
+  if (in_row_stride > (int64_t(1) << 40) / m || out_row_stride > (int64_t(1) << 40) / m)
+    return HADACORE_ERROR_TOO_LARGE;
+  // byte ranges of the input rows, the code rows and the scales must be disjoint
+  uintptr_t ilo, ihi;
+  row_span(in, in_row_stride, m, n, &ilo, &ihi);
+  const uintptr_t clo = reinterpret_cast<uintptr_t>(out_codes);
+  const uintptr_t chi = clo + (uintptr_t)((m - 1) * out_row_stride + n);
+  const uintptr_t slo = reinterpret_cast<uintptr_t>(out_scales);
+  const uintptr_t shi = slo + (uintptr_t)(4 * m);
+  if ((ilo < chi && clo < ihi) || (ilo < shi && slo < ihi) || (clo < shi && slo < chi))
+    return HADACORE_ERROR_OVERLAP;
+
+  const hadacore_status dev = check_device();
+  if (dev != HADACORE_SUCCESS) return dev;
+  const uint16_t *src = static_cast<const uint16_t *>(in);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const ScaleArgs sc = split_scale(scale, dtype);
+  const Fp8Out fp8{static_cast<uint8_t *>(out_codes), out_row_stride, out_scales};
+  const int front = front_override();
+  const hipError_t err =
+      dtype == HADACORE_FP16
+          ? launch_dt<HADACORE_FP16, kFp8>(L, src, in_row_stride, nullptr, 0, m, sc, front, s, fp8)
+          : launch_dt<HADACORE_BF16, kFp8>(L, src, in_row_stride, nullptr, 0, m, sc, front, s, fp8);
+  return err == hipSuccess ? HADACORE_SUCCESS : HADACORE_ERROR_LAUNCH;
 }
 
 extern "C" hadacore_status hadacore_stream_copy(const void *src, void *dst, int64_t bytes,

@@ -5,9 +5,10 @@ kernels of ``libhadacore.so``.  The library is loaded from this package
 directory; if it is missing, every call raises (there is no fallback).
 
 The raw entry points take device addresses as integers and keep the C names:
-``hadamard_transform``, ``hadamard_transform_strided``, ``hadacore_stream_copy``,
-``hadacore_status_string``, ``hadacore_version``.  ``transform`` is a
-convenience wrapper for 2-D torch tensors on a ROCm device.
+``hadamard_transform``, ``hadamard_transform_strided``, ``hadamard_transform_fp8``,
+``hadacore_stream_copy``, ``hadacore_status_string``, ``hadacore_version``.
+``transform`` and ``transform_fp8`` are convenience wrappers for 2-D torch
+tensors on a ROCm device.
 """
 from __future__ import annotations
 
@@ -25,8 +26,8 @@ STATUS_NAMES = {
     4: "INVALID_STRIDE", 5: "MISALIGNED", 6: "OVERLAP", 7: "LAUNCH",
     8: "UNSUPPORTED_DEVICE", 9: "TOO_LARGE",
 }
-EXPORTS = ("hadamard_transform", "hadamard_transform_strided", "hadacore_stream_copy",
-           "hadacore_status_string", "hadacore_version")
+EXPORTS = ("hadamard_transform", "hadamard_transform_strided", "hadamard_transform_fp8",
+           "hadacore_stream_copy", "hadacore_status_string", "hadacore_version")
 
 
 class HadacoreError(RuntimeError):
@@ -52,6 +53,8 @@ def library() -> ctypes.CDLL:
         lib.hadamard_transform.restype = i32
         lib.hadamard_transform_strided.argtypes = [vp, i64, vp, i64, i64, i64, i32, f32, vp]
         lib.hadamard_transform_strided.restype = i32
+        lib.hadamard_transform_fp8.argtypes = [vp, i64, vp, i64, vp, i64, i64, i32, f32, vp]
+        lib.hadamard_transform_fp8.restype = i32
         lib.hadacore_stream_copy.argtypes = [vp, vp, i64, vp]
         lib.hadacore_stream_copy.restype = i32
         lib.hadacore_status_string.argtypes = [i32]
@@ -82,6 +85,16 @@ def hadamard_transform_strided(in_ptr: int, in_row_stride: int, out_ptr: int,
                                               m, n, dtype, scale, stream)
     if check:
         _check(st, "hadamard_transform_strided")
+    return st
+
+
+def hadamard_transform_fp8(in_ptr: int, in_row_stride: int, codes_ptr: int, codes_row_stride: int,
+                           scales_ptr: int, m: int, n: int, dtype: int, scale: float,
+                           stream: int = 0, check: bool = True) -> int:
+    st = library().hadamard_transform_fp8(in_ptr, in_row_stride, codes_ptr, codes_row_stride,
+                                          scales_ptr, m, n, dtype, scale, stream)
+    if check:
+        _check(st, "hadamard_transform_fp8")
     return st
 
 
@@ -143,3 +156,38 @@ def transform(x, out=None, scale: float | None = None, n: int | None = None, str
         hadamard_transform_strided(x.data_ptr(), in_stride, out.data_ptr(), out_stride,
                                    x.shape[0], n, code, scale, stream)
     return out
+
+
+def transform_fp8(x, codes=None, scales=None, scale: float | None = None, stream=None):
+    """Fused transform + per-row e4m3 quantization of a 2-D float16/bfloat16 tensor.
+
+    Returns (codes, scales): codes is a (m, n) torch.uint8 tensor of e4m3 bit
+    patterns (view it as torch.float8_e4m3fn to decode) and scales a (m,)
+    float32 tensor, so that x @ H_n * scale ~ codes.float() * scales[:, None].
+    """
+    import torch
+    if x.dim() != 2 or not x.is_cuda or x.stride(1) != 1:
+        raise ValueError("expected a 2-D ROCm tensor with contiguous rows")
+    code = _dtype_code(x)
+    m, n = x.shape
+    if codes is None:
+        codes = torch.empty((m, n), dtype=torch.uint8, device=x.device)
+    if scales is None:
+        scales = torch.empty((m,), dtype=torch.float32, device=x.device)
+    if codes.dtype != torch.uint8 or codes.dim() != 2 or codes.stride(1) != 1 \
+            or tuple(codes.shape) != (m, n):
+        raise ValueError("codes must be a (m, n) uint8 tensor with contiguous rows")
+    if scales.dtype != torch.float32 or scales.numel() != m or not scales.is_contiguous():
+        raise ValueError("scales must be a contiguous float32 tensor of m elements")
+    if scale is None:
+        scale = float(ctypes.c_float(1.0 / math.sqrt(n)).value)
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device).cuda_stream
+    elif hasattr(stream, "cuda_stream"):
+        stream = stream.cuda_stream
+    in_stride = x.stride(0) if m > 1 else n
+    codes_stride = codes.stride(0) if m > 1 else ((n + 15) // 16) * 16
+    with torch.cuda.device(x.device):
+        hadamard_transform_fp8(x.data_ptr(), in_stride, codes.data_ptr(), codes_stride,
+                               scales.data_ptr(), m, n, code, scale, stream)
+    return codes, scales

@@ -1,0 +1,69 @@
+"""Comparison of fused FP8 results with the oracle.
+
+Codes are judged in the oracle's own decision variable v = y32 * (448/amax),
+y32 being the exact transform rounded once to fp32.  A GPU code must decode to
+the oracle's code, or -- where the GPU's fp32 transform (whose error is a small
+multiple of 2^-24 of the row's magnitudes) can land on the other side of a
+rounding boundary -- to a value within half an e4m3 step plus that error of v.
+Scales must agree within a few fp32 ulps.  -0 equals +0.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+REL_FP32_SLACK = 2.0 ** -17      # fp32 transform error allowance, relative to the row maximum
+SCALE_RTOL = 2.0 ** -19          # a few fp32 ulps
+MAX_MISMATCH_FRACTION = 1e-3
+
+
+def spacing_e4m3(v: np.ndarray) -> np.ndarray:
+    a = np.abs(np.asarray(v, dtype=np.float64))
+    with np.errstate(divide="ignore"):
+        e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    return np.where(a < 2.0 ** -6, 2.0 ** -9, np.exp2(e - 3))
+
+
+@dataclass
+class Fp8Comparison:
+    count: int
+    mismatches: int
+    invalid: int
+    scale_bad: int
+
+    @property
+    def ok(self) -> bool:
+        return (self.invalid == 0 and self.scale_bad == 0
+                and self.mismatches <= MAX_MISMATCH_FRACTION * max(self.count, 1))
+
+    def __str__(self) -> str:
+        return (f"fp8: n={self.count} code_mismatches={self.mismatches} invalid={self.invalid} "
+                f"scale_bad={self.scale_bad}")
+
+
+def compare_fp8(oracle, codes_gpu: np.ndarray, scales_gpu: np.ndarray, bits: np.ndarray,
+                dtype: str, scale: float, n: int) -> Fp8Comparison:
+    codes_o, scales_o = oracle.fwht_fp8(bits, dtype, scale, n=n)
+    y32 = oracle.fwht(bits, dtype, scale, n=n).astype(np.float32)
+    with np.errstate(all="ignore"):
+        amax = np.where(np.isnan(y32).all(axis=1), np.nan, np.nanmax(np.abs(y32), axis=1))
+        amax = amax.astype(np.float32)
+        inv = np.where(amax > 0, np.float32(448.0) / amax, np.float32(0.0)).astype(np.float32)
+        v = (y32 * inv[:, None]).astype(np.float64)
+    dg = oracle.decode_e4m3(codes_gpu[:, :n])
+    do = oracle.decode_e4m3(codes_o)
+    both_nan = np.isnan(dg) & np.isnan(do)
+    exact = (dg == do) | both_nan
+    with np.errstate(all="ignore"):
+        near = np.abs(dg - v) <= 0.5 * spacing_e4m3(v) + REL_FP32_SLACK * 448.0
+    valid = exact | (near & np.isfinite(dg))
+    sg = scales_gpu.astype(np.float64)
+    so = scales_o.astype(np.float64)
+    same_class = (np.isnan(sg) == np.isnan(so)) & (np.isinf(sg) == np.isinf(so))
+    with np.errstate(all="ignore"):
+        close = np.where(np.isfinite(so), np.abs(sg - so) <= SCALE_RTOL * np.abs(so), sg == so)
+    close = close | (np.isnan(sg) & np.isnan(so))
+    return Fp8Comparison(count=int(dg.size), mismatches=int(np.count_nonzero(~exact)),
+                         invalid=int(np.count_nonzero(~valid)),
+                         scale_bad=int(np.count_nonzero(~(same_class & close))))

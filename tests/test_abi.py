@@ -146,3 +146,32 @@ def test_errors_raise_in_python():
     with pytest.raises(H.HadacoreError) as e:
         H.hadamard_transform(A, B, 4, 100, H.FP16, 1.0, 0)
     assert e.value.status == 2
+
+
+def _fp8(*args):
+    return H.hadamard_transform_fp8(*args, check=False)
+
+
+C8 = 1 << 34   # fake codes buffer
+S8 = 1 << 35   # fake scales buffer
+
+
+@cpu_only
+def test_fp8_validation():
+    ok_args = (A, 128, C8, 128, S8, 4, 128, H.BF16, 1.0, 0)
+    assert _fp8(A, 128, C8, 128, S8, 4, 100, H.BF16, 1.0, 0) == 2          # size
+    assert _fp8(A, 128, C8, 128, S8, 4, 128, 5, 1.0, 0) == 3                # dtype
+    assert _fp8(A, 128, C8, 136, S8, 4, 128, H.BF16, 1.0, 0) == 4           # codes stride % 16
+    assert _fp8(A, 128, C8, 120, S8, 4, 128, H.BF16, 1.0, 0) == 4           # codes stride < n
+    assert _fp8(A, 120, C8, 128, S8, 4, 128, H.BF16, 1.0, 0) == 4           # input stride < n
+    assert _fp8(A, 128, C8 + 8, 128, S8, 4, 128, H.BF16, 1.0, 0) == 5       # codes alignment
+    assert _fp8(A, 128, C8, 128, S8 + 2, 4, 128, H.BF16, 1.0, 0) == 5       # scales alignment
+    assert _fp8(A, 128, 0, 128, S8, 4, 128, H.BF16, 1.0, 0) == 1            # null codes
+    assert _fp8(A, 128, C8, 128, 0, 4, 128, H.BF16, 1.0, 0) == 1            # null scales
+    assert _fp8(A, 128, C8, 128, S8, 4, 128, H.BF16, math.nan, 0) == 1      # scale
+    assert _fp8(A, 128, A + 64, 128, S8, 4, 128, H.BF16, 1.0, 0) == 6       # codes inside input
+    assert _fp8(A, 128, C8, 128, A + 16, 4, 128, H.BF16, 1.0, 0) == 6       # scales inside input
+    assert _fp8(A, 128, C8, 128, C8 + 256, 4, 128, H.BF16, 1.0, 0) == 6     # scales inside codes
+    assert _fp8(0, 128, 0, 128, 0, 0, 128, H.BF16, 1.0, 0) == 0             # m == 0
+    assert _fp8(A, 128, C8, 128, S8, -1, 128, H.BF16, 1.0, 0) == 1
+    assert len(ok_args) == 10
