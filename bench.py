@@ -182,8 +182,9 @@ def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0
     }
 
 
-def cpu_baseline(w, target_seconds: float) -> dict:
-    """The fp64 oracle on the host cores, timed on a bounded row sample of the workload."""
+def cpu_baseline(w, target_seconds: float, fp8: bool = False) -> dict:
+    """The fp64 oracle on the host cores, timed on a bounded row sample of the workload
+    (with fp8, the oracle's fused transform + e4m3 quantization, which runs on one thread)."""
     import numpy as np
     import oracle
     from paper_2412_08832_amd import workloads as W
@@ -191,12 +192,19 @@ def cpu_baseline(w, target_seconds: float) -> dict:
         cores = len(os.sched_getaffinity(0))
     except AttributeError:
         cores = os.cpu_count() or 1
-    cores = max(1, min(cores, 16))
+    cores = 1 if fp8 else max(1, min(cores, 16))
     orc = oracle.get()
-    probe_rows = max(1, min(w.m, (1 << 20) // w.n))
+
+    def run(b):
+        if fp8:
+            orc.fwht_fp8(b, w.dtype, w.scale)
+        else:
+            orc.fwht(b, w.dtype, w.scale, nthreads=cores)
+
+    probe_rows = max(1, min(w.m, (1 << 20) // w.n // (16 if fp8 else 1)))
     bits = W.generate(w, rows=probe_rows)
     t0 = time.perf_counter()
-    orc.fwht(bits, w.dtype, w.scale, nthreads=cores)
+    run(bits)
     rate = probe_rows * w.n / max(time.perf_counter() - t0, 1e-6)
     rows = int(min(w.m, max(probe_rows, target_seconds * rate / w.n)))
     bits = W.generate(w, rows=rows) if rows != probe_rows else bits
@@ -204,7 +212,7 @@ def cpu_baseline(w, target_seconds: float) -> dict:
     passes = 0
     t0 = time.perf_counter()
     while True:
-        orc.fwht(bits, w.dtype, w.scale, nthreads=cores)
+        run(bits)
         passes += 1
         sec = time.perf_counter() - t0
         if sec >= target_seconds or passes >= 1000:
@@ -221,7 +229,8 @@ def cpu_baseline(w, target_seconds: float) -> dict:
         "value": passes * rows * w.n / sec, "unit": "elements/s", "cores": cores, "kind": "oracle",
         "sample": f"{passes} pass(es) over the first {rows} of {w.m} rows ({rows * w.n} "
                   f"elements each), {sec:.1f} s, "
-                  f"fp64 iterative FWHT in C on {cores} threads, {cpu}",
+                  + ("fp64 iterative FWHT + e4m3 quantization in C on 1 thread, " if fp8 else
+                     f"fp64 iterative FWHT in C on {cores} threads, ") + cpu,
     }
 
 
@@ -279,7 +288,7 @@ def main(argv=None) -> int:
                       f"of peak, {100 * pr['frac_of_copy']:.1f}% of copy)", file=sys.stderr,
                       flush=True)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, fp8=args.fp8)
     print(json.dumps(line), flush=True)
     return 0
 

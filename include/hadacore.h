@@ -24,7 +24,9 @@
  * Memory: all pointers are DEVICE pointers owned by the caller; the library
  * never allocates, frees or retains them.  Rows are contiguous (element
  * stride 1) and start every `row_stride` elements; elements between n and the
- * row stride are neither read nor written.
+ * row stride are neither read nor written.  Row strides are at most 2^26
+ * elements (bytes for FP8 codes), which keeps every offset inside a group of
+ * rows handled by one wave below 2^32 bytes.
  *
  * Streams: work is enqueued asynchronously on `stream` (a hipStream_t; NULL
  * means the default stream) and the call returns without synchronizing.
@@ -63,7 +65,7 @@ typedef int32_t hadacore_status;
 #define HADACORE_ERROR_INVALID_VALUE 1      /* m < 0, null pointer with m > 0, non-finite scale */
 #define HADACORE_ERROR_INVALID_SIZE 2       /* n not a power of two in [128, 32768] */
 #define HADACORE_ERROR_INVALID_DTYPE 3      /* dtype not HADACORE_FP16 / HADACORE_BF16 */
-#define HADACORE_ERROR_INVALID_STRIDE 4     /* row stride < n, or not a multiple of 8 elements */
+#define HADACORE_ERROR_INVALID_STRIDE 4     /* row stride < n, > 2^26, or not a multiple of 8 */
 #define HADACORE_ERROR_MISALIGNED 5         /* in or out not 16-byte aligned */
 #define HADACORE_ERROR_OVERLAP 6            /* in/out overlap without being the same layout */
 #define HADACORE_ERROR_LAUNCH 7             /* the HIP runtime rejected the kernel launch */
@@ -90,7 +92,7 @@ hadacore_status hadamard_transform(const void *in, void *out, int64_t m, int64_t
 /*
  * hadamard_transform_strided -- as hadamard_transform, with row i of the input
  * at in + i*in_row_stride and row i of the output at out + i*out_row_stride
- * (strides in elements, each >= n and a multiple of 8).  In-place operation
+ * (strides in elements, each >= n, <= 2^26 and a multiple of 8).  In-place operation
  * requires in == out and in_row_stride == out_row_stride.
  */
 hadacore_status hadamard_transform_strided(const void *in, int64_t in_row_stride, void *out,
@@ -109,9 +111,9 @@ hadacore_status hadamard_transform_strided(const void *in, int64_t in_row_stride
  * so that y_j ~ decode_e4m3(out_codes[i][j]) * out_scales[i].  e4m3: 1 sign,
  * 4 exponent (bias 7) and 3 fraction bits, largest finite 448, 0x7f NaN.
  *   in              device pointer, m rows of n 16-bit values at in_row_stride
- *                   elements (>= n, multiple of 8), 16-byte aligned
+ *                   elements (>= n, <= 2^26, multiple of 8), 16-byte aligned
  *   out_codes       device pointer, m rows of n bytes at out_row_stride bytes
- *                   (>= n, multiple of 16), 16-byte aligned
+ *                   (>= n, <= 2^26, multiple of 16), 16-byte aligned
  *   out_scales      device pointer to m floats, 4-byte aligned
  * The three ranges must not overlap (OVERLAP otherwise).  Other arguments,
  * streams, ownership and errors as for hadamard_transform.

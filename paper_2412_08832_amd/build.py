@@ -26,6 +26,8 @@ HIPCC_FLAGS = [
     "-Wall",
     # keep fp32 math unpacked (no v_pk_*_f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core results straight into VGPRs (no accumulation-register reads)
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-fno-gpu-rdc",
 ]
 

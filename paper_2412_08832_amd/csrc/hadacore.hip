@@ -97,6 +97,19 @@ __device__ __forceinline__ void gstore(uint16_t *p, u4 v) {
   }
 }
 
+// The same at base + byte offset.  With a wave-uniform base and a 32-bit
+// offset this is one global access with the base in scalar registers and no
+// per-lane 64-bit address arithmetic.
+template <bool NT>
+__device__ __forceinline__ u4 gload_at(const void *base, uint32_t off) {
+  return gload<NT>(reinterpret_cast<const uint16_t *>(static_cast<const char *>(base) + off));
+}
+
+template <bool NT>
+__device__ __forceinline__ void gstore_at(void *base, uint32_t off, u4 v) {
+  gstore<NT>(reinterpret_cast<uint16_t *>(static_cast<char *>(base) + off), v);
+}
+
 // ---- 16-bit <-> fp32 ------------------------------------------------------
 
 // Widens the packed pair in `u` (element 2i in the low half), multiplies by
@@ -173,7 +186,8 @@ __device__ __forceinline__ void reg_stage(float (&v)[N]) {
 template <int LB, int N>
 __device__ __forceinline__ void lane_stage(float (&v)[N], int lane) {
   static_assert(N % 8 == 0, "registers come in chunks of 8");
-  const float sgn = (lane & (1 << LB)) ? -1.0f : 1.0f;
+  const float sgn = __builtin_bit_cast(
+      float, 0x3F800000u | (((uint32_t)lane << (31 - LB)) & 0x80000000u));  // -1 iff bit LB
   if constexpr (LB == 0) {
 #pragma unroll
     for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("quad_perm:[1,0,3,2]");
@@ -280,23 +294,45 @@ __device__ __forceinline__ void widen_chunks(const u4 (&raw)[C], float (&v)[C * 
   }
 }
 
-// MFMA A operand for lane l: 8 consecutive 16-bit entries of row (l & 15) (top)
-// or 16 + (l & 15) (bottom) of H_32 * 2^e, columns 8*(l >> 4) .. +7.
-// H_32[r][c] = (-1)^popcount(r & c); bf16 entries carry 2^e in their exponent.
-template <int DT>
-__device__ __forceinline__ u4 h32_operand(int lane, int e2, int bottom) {
-  const int m = lane & 15;
-  const int g = lane >> 4;
-  const int base = (__builtin_popcount(m & (8 * g)) + (bottom & (g >> 1))) & 1;
-  const uint32_t one = DT == HADACORE_FP16 ? 0x3C00u : (uint32_t)(0x3F80 + e2 * 128);
-  u4 r;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const uint32_t s0 = (uint32_t)(base ^ __builtin_popcount(m & (2 * q))) & 1u;
-    const uint32_t s1 = (uint32_t)(base ^ __builtin_popcount(m & (2 * q + 1))) & 1u;
-    r[q] = (one | (s0 << 15)) | ((one | (s1 << 15)) << 16);
+// MFMA A operands: lane l holds 8 consecutive 16-bit entries, columns
+// 8*(l >> 4) .. +7, of row (l & 15) (top) and of row 16 + (l & 15) (bottom) of
+// H_32 * 2^e, where H_32[r][c] = (-1)^popcount(r & c).  The sign bits depend
+// on the lane only and come from a 2 KiB table (words 0-3 top, 4-7 bottom);
+// the magnitude 2^e (fp16: 1) is OR-ed in per call.
+struct H32Signs {
+  uint32_t w[kWave][8];
+};
+
+constexpr int parity_of(int x) {
+  int p = 0;
+  for (; x != 0; x &= x - 1) p ^= 1;
+  return p;
+}
+
+constexpr H32Signs make_h32_signs() {
+  H32Signs t{};
+  for (int l = 0; l < kWave; ++l) {
+    for (int half = 0; half < 2; ++half) {
+      const int r = 16 * half + (l & 15);
+      for (int q = 0; q < 4; ++q) {
+        const int c = 8 * (l >> 4) + 2 * q;
+        t.w[l][4 * half + q] = (parity_of(r & c) ? 0x8000u : 0u) |
+                               (parity_of(r & (c + 1)) ? 0x80000000u : 0u);
+      }
+    }
   }
-  return r;
+  return t;
+}
+
+__device__ const H32Signs kH32Signs = make_h32_signs();
+
+template <int DT>
+__device__ __forceinline__ void h32_operands(int lane, int e2, u4 &top, u4 &bot) {
+  const uint32_t one = DT == HADACORE_FP16 ? 0x3C00u : (uint32_t)(0x3F80 + e2 * 128);
+  const uint32_t mag = one | (one << 16);
+  const u4 *p = reinterpret_cast<const u4 *>(kH32Signs.w[lane]);
+  top = p[0] | mag;
+  bot = p[1] | mag;
 }
 
 // Radix-32 step of one chunk on the matrix cores (kMfma front).
@@ -336,8 +372,8 @@ __device__ __forceinline__ void front(const u4 (&raw)[C], float (&v)[C * 8], int
     reg_stage<1>(v);
     reg_stage<2>(v);
   } else {
-    const u4 a_top = h32_operand<DT>(lane, e2, 0);
-    const u4 a_bot = h32_operand<DT>(lane, e2, 1);
+    u4 a_top, a_bot;
+    h32_operands<DT>(lane, e2, a_top, a_bot);
 #pragma unroll
     for (int k = 0; k < C; ++k) mfma_front<DT>(raw[k], a_top, a_bot, &v[k * 8]);
   }
@@ -415,38 +451,35 @@ struct Fp8Out {
 
 typedef uint32_t u2 __attribute__((ext_vector_type(2)));
 
-// Value of `x` held by lane (lane ^ (1 << LB)).
-template <int LB>
-__device__ __forceinline__ float lane_partner(float x, int lane) {
-  const int xi = __builtin_bit_cast(int, x);
-  int r;
-  if constexpr (LB == 0) {
-    r = __builtin_amdgcn_mov_dpp(xi, 0xB1, 0xF, 0xF, true);   // quad_perm:[1,0,3,2]
-  } else if constexpr (LB == 1) {
-    r = __builtin_amdgcn_mov_dpp(xi, 0x4E, 0xF, 0xF, true);   // quad_perm:[2,3,0,1]
-  } else if constexpr (LB == 2) {
-    r = __builtin_amdgcn_ds_swizzle(xi, 0x101F);              // xor 4
-  } else if constexpr (LB == 3) {
-    r = __builtin_amdgcn_mov_dpp(xi, 0x128, 0xF, 0xF, true);  // row_ror:8 == xor 8
-  } else if constexpr (LB == 4) {
-    r = __builtin_amdgcn_ds_swizzle(xi, 0x401F);              // xor 16
-  } else {
-    r = __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, xi);   // xor 32
-  }
-  return __builtin_bit_cast(float, r);
-}
+// Maximum of x over the lanes that differ from this one only in the lane
+// bits of MASK.  Every operand is a result of arithmetic, so NaNs are quiet
+// and a plain v_max_f32 -- which returns the number when the other operand is
+// a quiet NaN -- is the maxNum of the definition.  It is written in asm so
+// that the compiler adds no canonicalizing v_max per step; the DPP forms fold
+// the exchange into the max.  The leading s_nop 1 gives the two wait states a
+// DPP read needs after a VALU write of its register.  Requires all lanes active.
+#define HC_MAX_DPP(CTRL) \
+  asm("s_nop 1\n\tv_max_f32_dpp %0, %0, %0 " CTRL " row_mask:0xf bank_mask:0xf" : "+v"(x))
 
-// Maximum over the lanes that differ from this one only in the lane bits of MASK.
-template <int MASK>
-__device__ __forceinline__ float lane_max(float x, int lane) {
-  if constexpr ((MASK & 1) != 0) x = fmaxf(x, lane_partner<0>(x, lane));
-  if constexpr ((MASK & 2) != 0) x = fmaxf(x, lane_partner<1>(x, lane));
-  if constexpr ((MASK & 4) != 0) x = fmaxf(x, lane_partner<2>(x, lane));
-  if constexpr ((MASK & 8) != 0) x = fmaxf(x, lane_partner<3>(x, lane));
-  if constexpr ((MASK & 16) != 0) x = fmaxf(x, lane_partner<4>(x, lane));
-  if constexpr ((MASK & 32) != 0) x = fmaxf(x, lane_partner<5>(x, lane));
+__device__ __forceinline__ float max_with(float x, int partner_bits) {
+  asm("v_max_f32 %0, %0, %1" : "+v"(x) : "v"(partner_bits));
   return x;
 }
+
+template <int MASK>
+__device__ __forceinline__ float lane_max(float x, int lane) {
+  if constexpr ((MASK & 1) != 0) HC_MAX_DPP("quad_perm:[1,0,3,2]");
+  if constexpr ((MASK & 2) != 0) HC_MAX_DPP("quad_perm:[2,3,0,1]");
+  if constexpr ((MASK & 4) != 0)
+    x = max_with(x, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x101F));  // xor 4
+  if constexpr ((MASK & 8) != 0) HC_MAX_DPP("row_ror:8");                                 // xor 8
+  if constexpr ((MASK & 16) != 0)
+    x = max_with(x, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));  // xor 16
+  if constexpr ((MASK & 32) != 0)
+    x = max_with(x, __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __builtin_bit_cast(int, x)));
+  return x;
+}
+#undef HC_MAX_DPP
 
 // Lane bits along which one row's elements are spread after the stages.
 template <int FRONT, int L>
@@ -454,10 +487,13 @@ constexpr int row_lane_mask() {
   return FRONT == kValu ? lane_stage_mask<kValu, L>() : (lane_stage_mask<kMfma, L>() | 0x30);
 }
 
+// max |v[j]| over 8 registers (maxNum: quiet NaNs lose), 4 instructions.
 __device__ __forceinline__ float abs_max8(const float *v) {
-  float a = fabsf(v[0]);
-#pragma unroll
-  for (int j = 1; j < 8; ++j) a = fmaxf(a, fabsf(v[j]));
+  float a;
+  asm("v_max3_f32 %0, |%1|, |%2|, |%3|" : "=v"(a) : "v"(v[0]), "v"(v[1]), "v"(v[2]));
+  asm("v_max3_f32 %0, %0, |%1|, |%2|" : "+v"(a) : "v"(v[3]), "v"(v[4]));
+  asm("v_max3_f32 %0, %0, |%1|, |%2|" : "+v"(a) : "v"(v[5]), "v"(v[6]));
+  asm("v_max_f32_e64 %0, %0, |%1|" : "+v"(a) : "v"(v[7]));
   return a;
 }
 
@@ -471,8 +507,8 @@ __device__ __forceinline__ u2 to_e4m3x8(const float *v, float mul) {
 }
 
 template <bool NT>
-__device__ __forceinline__ void gstore8(uint8_t *p, u2 v) {
-  u2 *q = reinterpret_cast<u2 *>(p);
+__device__ __forceinline__ void gstore8_at(void *base, uint32_t off, u2 v) {
+  u2 *q = reinterpret_cast<u2 *>(static_cast<char *>(base) + off);
   if constexpr (NT) {
     __builtin_nontemporal_store(v, q);
   } else {
@@ -480,18 +516,25 @@ __device__ __forceinline__ void gstore8(uint8_t *p, u2 v) {
   }
 }
 
-// Quantization multiplier of a lane: the twist sign (and, for kMfma, the part
-// of the scale the front end left out) times 448/amax; amax is the row's
-// largest |y| given the largest |register| of the row.
+// Row scale and quantization multiplier of a lane, given the largest |register|
+// of its row.  The multiplier includes the twist sign (and, for kMfma, the part
+// of the scale the front end left out).  Both correctly rounded quotients come
+// from one division: even lanes form 448 / amax, odd lanes amax / 448, and the
+// pair swaps them (lanes 2i and 2i+1 always hold the same row).  Requires all
+// lanes active.
 template <int FRONT>
 struct Fp8Quant {
-  float amax;
-  float mul;
-  __device__ __forceinline__ Fp8Quant(float reg_amax, bool tw, float post) {
+  float scale;  // amax / 448
+  float mul;    // (twist sign) * (kMfma: post) * 448 / amax, 0 for a zero row
+  __device__ __forceinline__ Fp8Quant(float reg_amax, bool tw, float post, int lane) {
     const float mag = FRONT == kMfma ? fabsf(post) : 1.0f;
-    amax = reg_amax * mag;
-    const float inv = amax > 0.0f ? 448.0f / amax : 0.0f;
-    // true value = register * (twist sign) * (kMfma: post), quantized as true * inv
+    const float amax = reg_amax * mag;
+    const bool odd = (lane & 1) != 0;
+    const float q = (odd ? amax : 448.0f) / (odd ? 448.0f : amax);
+    const float qp = __builtin_bit_cast(
+        float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, q), 0xB1, 0xF, 0xF, true));
+    const float inv = amax > 0.0f ? (odd ? qp : q) : 0.0f;
+    scale = odd ? q : qp;
     const float to_true = FRONT == kMfma ? (tw ? -post : post) : (tw ? -1.0f : 1.0f);
     mul = to_true * inv;
   }
@@ -504,7 +547,9 @@ struct Fp8Quant {
 // loading tile t+1 while it computes tile t, so that per-wave setup (operand
 // constants, signs, addressing) is paid once per T tiles while only one or two
 // tiles per wave are in flight.  WPB independent waves per workgroup.  Only
-// the last tile can end past row m; it masks those rows.
+// the last tile can end past row m; it masks those rows.  Addresses are a
+// wave-uniform tile base plus per-lane byte offsets inside the tile, which the
+// row stride limit (2^26 elements) keeps below 2^32.
 template <int DT, int L, int C, int T, int WPB, bool NT, int FRONT, int EPI>
 __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
     const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, int64_t m,
@@ -512,43 +557,63 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
   constexpr int kTile = 512 * C;
   static_assert((1 << L) <= kTile, "row does not fit a wave tile");
   constexpr int kRows = kTile >> L;
+  static_assert(kRows <= 32, "in-tile offsets must stay below 2^32 bytes");
   constexpr int kMask = (1 << L) - 1;
   const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   int64_t row0 = ((int64_t)blockIdx.x * WPB + wave) * (int64_t)(T * kRows);
   if (row0 >= m) return;
+
   const int lf_load = lane_field_load<FRONT, L>(lane);
   const int lf = lane_field<FRONT, L>(lane);
+  const int64_t out_pitch = EPI == kStore16 ? out_stride * 2 : fp8.stride;  // bytes per row
+  int ld_row[C], st_row[C];
+  uint32_t ld_off[C], st_off[C];
+#pragma unroll
+  for (int k = 0; k < C; ++k) {
+    const int tl = (k * kWave + lf_load) * 8;
+    ld_row[k] = tl >> L;
+    ld_off[k] = (uint32_t)ld_row[k] * (uint32_t)(in_stride * 2) + (uint32_t)(tl & kMask) * 2u;
+    const int ts = (k * kWave + lf) * 8;
+    st_row[k] = ts >> L;
+    st_off[k] = (uint32_t)st_row[k] * (uint32_t)out_pitch +
+                (uint32_t)(ts & kMask) * (EPI == kStore16 ? 2u : 1u);
+  }
   const Finisher<DT, FRONT> fin(twisted<FRONT, L>(lane), sc.post);
   u4 a_top = {0, 0, 0, 0}, a_bot = {0, 0, 0, 0};
-  if constexpr (FRONT == kMfma) {
-    a_top = h32_operand<DT>(lane, sc.e2, 0);
-    a_bot = h32_operand<DT>(lane, sc.e2, 1);
-  }
+  if constexpr (FRONT == kMfma) h32_operands<DT>(lane, sc.e2, a_top, a_bot);
 
-  auto load_tile = [&](int64_t r0, u4 (&raw)[C]) {
-    const bool full = r0 + kRows <= m;
-    const uint16_t *src = in + r0 * in_stride;
+  const char *src = reinterpret_cast<const char *>(in) + row0 * in_stride * 2;
+  char *dst = EPI == kStore16 ? reinterpret_cast<char *>(out) + row0 * out_pitch
+                              : reinterpret_cast<char *>(fp8.codes) + row0 * out_pitch;
+  float *scales = EPI == kStore16 ? nullptr : fp8.scales + row0;
+  auto rows_in_tile = [&](int64_t r0) { return (int)(m - r0 < kRows ? m - r0 : kRows); };
+  auto load_tile = [&](const char *base, int valid, u4(&raw)[C]) {
 #pragma unroll
     for (int k = 0; k < C; ++k) {
-      const int t = (k * kWave + lf_load) * 8;
-      if (full || r0 + (t >> L) < m) {
-        raw[k] = gload<NT>(src + (int64_t)(t >> L) * in_stride + (t & kMask));
+      if (kRows == 1 || ld_row[k] < valid) {
+        raw[k] = gload_at<NT>(base, ld_off[k]);
       } else {
         raw[k] = u4{0, 0, 0, 0};
       }
     }
   };
 
+  int valid = rows_in_tile(row0);
   u4 next[C];
-  load_tile(row0, next);
+  load_tile(src, valid, next);
 #pragma unroll 1
   for (int it = 0; it < T; ++it) {
     u4 raw[C];
 #pragma unroll
     for (int k = 0; k < C; ++k) raw[k] = next[k];
+    const int cur_valid = valid;
     const bool more = it + 1 < T && row0 + kRows < m;
-    if (more) load_tile(row0 + kRows, next);
+    if (more) {
+      src += (int64_t)kRows * in_stride * 2;
+      valid = rows_in_tile(row0 + kRows);
+      load_tile(src, valid, next);
+    }
     float v[C * 8];
     if constexpr (FRONT == kValu) {
       widen_chunks<DT, C>(raw, v, sc.scale);
@@ -559,53 +624,50 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
       for (int k = 0; k < C; ++k) mfma_front<DT>(raw[k], a_top, a_bot, &v[k * 8]);
     }
     wave_stages<FRONT, L, C>(v, lane);
-    const bool full = row0 + kRows <= m;
     if constexpr (EPI == kStore16) {
-      uint16_t *dst = out + row0 * out_stride;
 #pragma unroll
       for (int k = 0; k < C; ++k) {
-        const int t = (k * kWave + lf) * 8;
-        if (full || row0 + (t >> L) < m) {
-          gstore<NT>(dst + (int64_t)(t >> L) * out_stride + (t & kMask), fin(&v[k * 8]));
-        }
+        if (kRows == 1 || st_row[k] < cur_valid) gstore_at<NT>(dst, st_off[k], fin(&v[k * 8]));
       }
     } else {
-      // row maxima: within each chunk, across the chunks of one row, across its lanes
+      // row maxima: within each chunk, across the chunks of one row (chunk
+      // bits that are element bits), then across the row's lanes
+      constexpr int kChunkRow = (C >= 2 && L > 9 ? 1 : 0) | (C >= 4 && L > 10 ? 2 : 0) |
+                                (C >= 8 && L > 11 ? 4 : 0);
       float a[C];
 #pragma unroll
       for (int k = 0; k < C; ++k) a[k] = abs_max8(&v[k * 8]);
-      constexpr int kChunkRow = (C >= 2 && L > 9 ? 1 : 0) | (C >= 4 && L > 10 ? 2 : 0) |
-                                (C >= 8 && L > 11 ? 4 : 0);
 #pragma unroll
-      for (int bit = 1; bit < C; bit <<= 1) {
-        if ((kChunkRow & bit) != 0) {
+      for (int k = 0; k < C; ++k) {
+        if ((k & kChunkRow) == 0) {
 #pragma unroll
-          for (int k = 0; k < C; ++k) {
-            if ((k & bit) == 0) {
-              const float x = fmaxf(a[k], a[k | bit]);
-              a[k] = x;
-              a[k | bit] = x;
-            }
+          for (int j = 1; j < C; ++j) {
+            if ((j & ~kChunkRow) == 0) a[k] = max_with(a[k], __builtin_bit_cast(int, a[k | j]));
           }
         }
       }
       const bool tw = twisted<FRONT, L>(lane);
-      uint8_t *dst = fp8.codes + row0 * fp8.stride;
 #pragma unroll
       for (int k = 0; k < C; ++k) {
-        const int t = (k * kWave + lf) * 8;
-        const Fp8Quant<FRONT> qz(lane_max<row_lane_mask<FRONT, L>()>(a[k], lane), tw, sc.post);
-        if (full || row0 + (t >> L) < m) {
-          gstore8<NT>(dst + (int64_t)(t >> L) * fp8.stride + (t & kMask),
-                      to_e4m3x8(&v[k * 8], qz.mul));
-          if ((lane & row_lane_mask<FRONT, L>()) == 0 && (k & kChunkRow) == 0) {
-            fp8.scales[row0 + (t >> L)] = qz.amax / 448.0f;
+        if ((k & kChunkRow) != 0) continue;  // same row as chunk k & ~kChunkRow
+        const Fp8Quant<FRONT> qz(lane_max<row_lane_mask<FRONT, L>()>(a[k], lane), tw, sc.post,
+                                 lane);
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+          if ((j & ~kChunkRow) != k) continue;
+          if (kRows == 1 || st_row[j] < cur_valid) {
+            gstore8_at<NT>(dst, st_off[j], to_e4m3x8(&v[j * 8], qz.mul));
           }
+        }
+        if ((lane & row_lane_mask<FRONT, L>()) == 0 && (kRows == 1 || st_row[k] < cur_valid)) {
+          scales[st_row[k]] = qz.scale;
         }
       }
     }
     if (!more) break;
     row0 += kRows;
+    dst += (int64_t)kRows * out_pitch;
+    if constexpr (EPI != kStore16) scales += kRows;
   }
 }
 
@@ -630,15 +692,16 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   constexpr int kParts = 2 / HALVES;
   __shared__ float4 lds[n / 4 / HALVES];
   const int lane = threadIdx.x & (kWave - 1);
-  const int w = threadIdx.x / kWave;
+  const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   const int64_t row = blockIdx.x;
   const uint16_t *src = in + row * in_stride;
-  uint16_t *dst = EPI == kStore16 ? out + row * out_stride : nullptr;
 
   u4 raw[C];
   const int lf_load = lane_field_load<FRONT, L>(lane);
 #pragma unroll
-  for (int k = 0; k < C; ++k) raw[k] = gload<NT>(src + ((w * C + k) * kWave + lf_load) * 8);
+  for (int k = 0; k < C; ++k) {
+    raw[k] = gload_at<NT>(src, (uint32_t)(((w * C + k) * kWave + lf_load) * 16));
+  }
   float v[C * 8];
   front<DT, FRONT, C>(raw, v, lane, sc.scale, sc.e2);
   wave_stages<FRONT, L, C>(v, lane);
@@ -678,31 +741,32 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   const int lf = lane_field<FRONT, L>(lane);
   if constexpr (EPI == kStore16) {
     const Finisher<DT, FRONT> fin(twisted<FRONT, L>(lane), sc.post);
+    uint16_t *dst = out + row * out_stride;
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const int W = (k % NW) * C + (k / NW) * NW + w;
-      gstore<NT>(dst + (W * kWave + lf) * 8, fin(&v[k * 8]));
+      gstore_at<NT>(dst, (uint32_t)((W * kWave + lf) * 16), fin(&v[k * 8]));
     }
   } else {
     // the row spans the workgroup: registers, then lanes, then waves (through LDS)
     __shared__ float wave_max[NW];
     float a = abs_max8(&v[0]);
 #pragma unroll
-    for (int k = 1; k < C; ++k) a = fmaxf(a, abs_max8(&v[k * 8]));
+    for (int k = 1; k < C; ++k) a = max_with(a, __builtin_bit_cast(int, abs_max8(&v[k * 8])));
     a = lane_max<0x3F>(a, lane);
     if (lane == 0) wave_max[w] = a;
     __syncthreads();
     a = wave_max[0];
 #pragma unroll
     for (int i = 1; i < NW; ++i) a = fmaxf(a, wave_max[i]);
-    const Fp8Quant<FRONT> qz(a, twisted<FRONT, L>(lane), sc.post);
+    const Fp8Quant<FRONT> qz(a, twisted<FRONT, L>(lane), sc.post, lane);
     uint8_t *codes = fp8.codes + row * fp8.stride;
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const int W = (k % NW) * C + (k / NW) * NW + w;
-      gstore8<NT>(codes + (W * kWave + lf) * 8, to_e4m3x8(&v[k * 8], qz.mul));
+      gstore8_at<NT>(codes, (uint32_t)((W * kWave + lf) * 8), to_e4m3x8(&v[k * 8], qz.mul));
     }
-    if (threadIdx.x == 0) fp8.scales[row] = qz.amax / 448.0f;
+    if (threadIdx.x == 0) fp8.scales[row] = qz.scale;
   }
 }
 
@@ -753,42 +817,70 @@ hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int6
   return hipGetLastError();
 }
 
-// Per-size configuration, chosen from sustained HBM throughput measured on
-// MI355X (2^28-element in-place sweeps over chunks per lane, tiles per wave,
-// exchange passes, cache policy and front end, interleaved so that every
-// candidate sees the same clock state).  The smallest per-wave footprint that
-// holds a row wins up to n = 2048; from n = 4096 a row spreads over several
-// waves with one LDS exchange.  The matrix-core front end wins from n = 2048
-// on (except 16384); below that the VALU front is as fast and simpler.
-// `front` < 0 takes the table's choice; kValu / kMfma force one front end.
+// Launch configuration of one (size, epilogue, front end).
+struct Cfg {
+  int C;       // chunks of 8 elements per lane
+  int T;       // tiles per wave (wave kernel)
+  int WPB;     // waves per workgroup (wave kernel)
+  int HALVES;  // LDS exchange passes (block kernel)
+};
+
+// Per-size configurations, chosen from sustained HBM throughput measured on
+// MI355X (2^28-element sweeps over chunks per lane, tiles per wave, waves per
+// workgroup, exchange passes and front end, interleaved so that every
+// candidate sees the same clock state).  16-bit output: the smallest per-wave
+// footprint that holds a row wins up to n = 2048, and from n = 4096 a row
+// spreads over the waves of a workgroup with one LDS exchange.  FP8 output
+// has more arithmetic per byte, so small rows amortize the per-wave setup and
+// the row reduction over two tiles or chunks per wave, and n = 4096 stays in
+// one wave.
+template <int L, int EPI, int FRONT>
+constexpr Cfg config() {
+  if constexpr (EPI == kStore16) {
+    if constexpr (L <= 9) return {1, 1, 1, 1};
+    if constexpr (L == 10) return {2, 1, 1, 1};
+    if constexpr (L == 11 || L == 12) return {4, 1, 1, 1};
+    if constexpr (L == 13) return {4, 1, 1, FRONT == kMfma ? 1 : 2};
+    if constexpr (L == 14) return {8, 1, 1, FRONT == kMfma ? 1 : 2};
+    return {8, 1, 1, 2};
+  } else if constexpr (FRONT == kMfma) {
+    if constexpr (L == 7) return {2, 1, 1, 1};
+    if constexpr (L == 8 || L == 9) return {1, 4, 1, 1};
+    if constexpr (L == 10) return {2, 1, 1, 1};
+    if constexpr (L == 11 || L == 12) return {8, 1, 1, 1};
+    return {8, 1, 1, 2};
+  } else {
+    if constexpr (L <= 9) return {2, 1, 1, 1};
+    if constexpr (L == 10 || L == 11) return {4, 1, 1, 1};
+    if constexpr (L == 12) return {8, 1, 1, 1};
+    if constexpr (L == 13) return {4, 1, 1, 2};
+    return {8, 1, 1, 2};
+  }
+}
+
+// Front end used unless HADACORE_VARIANT forces one: the matrix cores from
+// n = 2048 for 16-bit output, everywhere for FP8 output.
+template <int L, int EPI>
+constexpr int default_front() {
+  return (EPI == kFp8 || L >= 11) ? kMfma : kValu;
+}
+
+template <int DT, int L, int EPI, int FRONT>
+hipError_t launch_front(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
+                        int64_t m, const ScaleArgs &sc, hipStream_t stream, Fp8Out fp8) {
+  constexpr Cfg c = config<L, EPI, FRONT>();
+  return launch_cfg<DT, L, c.C, c.T, c.WPB, c.HALVES, FRONT, EPI>(in, in_stride, out, out_stride,
+                                                                  m, sc, stream, fp8);
+}
+
+// `front` < 0 takes the default; kValu / kMfma force one front end.
 template <int DT, int L, int EPI>
 hipError_t launch(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
                   int64_t m, const ScaleArgs &sc, int front, hipStream_t stream, Fp8Out fp8) {
-  //                             default front       C  T  WPB HALVES
-  constexpr int kDefault = (L >= 11 && L != 14) ? kMfma : kValu;
-  const bool mfma = front < 0 ? kDefault == kMfma : front == kMfma;
-#define HC_CFG(C, T, WPB, H)                                                                     \
-  (mfma ? launch_cfg<DT, L, C, T, WPB, H, kMfma, EPI>(in, in_stride, out, out_stride, m, sc,      \
-                                                     stream, fp8)                                 \
-        : launch_cfg<DT, L, C, T, WPB, H, kValu, EPI>(in, in_stride, out, out_stride, m, sc,      \
-                                                     stream, fp8))
-  if constexpr (L <= 9) {
-    return HC_CFG(1, 1, 1, 1);
-  } else if constexpr (L == 10) {
-    return HC_CFG(2, 1, 1, 1);
-  } else if constexpr (L == 11) {
-    return HC_CFG(4, 1, 1, 1);
-  } else if constexpr (L == 12) {
-    return HC_CFG(4, 1, 1, 1);
-  } else if constexpr (L == 13) {
-    return mfma ? launch_cfg<DT, L, 4, 1, 1, 1, kMfma, EPI>(in, in_stride, out, out_stride, m, sc,
-                                                           stream, fp8)
-                : launch_cfg<DT, L, 4, 1, 1, 2, kValu, EPI>(in, in_stride, out, out_stride, m, sc,
-                                                           stream, fp8);
-  } else {
-    return HC_CFG(8, 1, 1, 2);
-  }
-#undef HC_CFG
+  const int f = front < 0 ? default_front<L, EPI>() : front;
+  return f == kMfma
+             ? launch_front<DT, L, EPI, kMfma>(in, in_stride, out, out_stride, m, sc, stream, fp8)
+             : launch_front<DT, L, EPI, kValu>(in, in_stride, out, out_stride, m, sc, stream, fp8);
 }
 
 template <int DT, int EPI = kStore16>
@@ -838,6 +930,10 @@ hadacore_status check_device() {
   return ok ? HADACORE_SUCCESS : HADACORE_ERROR_UNSUPPORTED_DEVICE;
 }
 
+// Largest row stride (elements, or bytes for FP8 codes): keeps every offset
+// inside a wave tile (at most 32 rows) below 2^32 bytes.
+constexpr int64_t kMaxStride = int64_t(1) << 26;
+
 int log2_exact(int64_t n) {
   if (n <= 0 || (n & (n - 1)) != 0) return -1;
   int l = 0;
@@ -861,7 +957,7 @@ hadacore_status validate(const void *in, int64_t in_row_stride, const void *out,
   if (dtype != HADACORE_FP16 && dtype != HADACORE_BF16) return HADACORE_ERROR_INVALID_DTYPE;
   if (!isfinite(scale)) return HADACORE_ERROR_INVALID_VALUE;
   if (in_row_stride < n || out_row_stride < n || (in_row_stride % 8) != 0 ||
-      (out_row_stride % 8) != 0)
+      (out_row_stride % 8) != 0 || in_row_stride > kMaxStride || out_row_stride > kMaxStride)
     return HADACORE_ERROR_INVALID_STRIDE;
   *L_out = L;
   if (m == 0) return HADACORE_SUCCESS;
@@ -922,7 +1018,7 @@ extern "C" hadacore_status hadamard_transform_fp8(const void *in, int64_t in_row
   if (dtype != HADACORE_FP16 && dtype != HADACORE_BF16) return HADACORE_ERROR_INVALID_DTYPE;
   if (!isfinite(scale)) return HADACORE_ERROR_INVALID_VALUE;
   if (in_row_stride < n || (in_row_stride % 8) != 0 || out_row_stride < n ||
-      (out_row_stride % 16) != 0)
+      (out_row_stride % 16) != 0 || in_row_stride > kMaxStride || out_row_stride > kMaxStride)
     return HADACORE_ERROR_INVALID_STRIDE;
   if (m == 0) return HADACORE_SUCCESS;
   if (in == nullptr || out_codes == nullptr || out_scales == nullptr)
@@ -983,7 +1079,8 @@ extern "C" const char *hadacore_status_string(hadacore_status status) {
     case HADACORE_ERROR_INVALID_VALUE: return "invalid value (m < 0, null pointer or non-finite scale)";
     case HADACORE_ERROR_INVALID_SIZE: return "invalid size (n must be a power of two in [128, 32768])";
     case HADACORE_ERROR_INVALID_DTYPE: return "invalid dtype (expected HADACORE_FP16 or HADACORE_BF16)";
-    case HADACORE_ERROR_INVALID_STRIDE: return "invalid row stride (must be >= n and a multiple of 8)";
+    case HADACORE_ERROR_INVALID_STRIDE:
+      return "invalid row stride (must be >= n, a multiple of 8 (16 for FP8 codes) and <= 2^26)";
     case HADACORE_ERROR_MISALIGNED: return "misaligned pointer (16-byte alignment required)";
     case HADACORE_ERROR_OVERLAP: return "input and output overlap without being the same layout";
     case HADACORE_ERROR_LAUNCH: return "kernel launch failed";

@@ -96,6 +96,10 @@ def test_invalid_strides():
     assert _st(A, 120, B, 128, 4, 128, H.FP16, 1.0, 0) == 4     # in stride < n
     assert _st(A, 128, B, 64, 4, 128, H.FP16, 1.0, 0) == 4      # out stride < n
     assert _st(A, 132, B, 128, 4, 128, H.FP16, 1.0, 0) == 4     # not a multiple of 8
+    big = (1 << 26) + 8                                          # above the 2^26 stride limit
+    assert _st(A, big, B, 128, 4, 128, H.FP16, 1.0, 0) == 4
+    assert _st(A, 128, B, big, 4, 128, H.BF16, 1.0, 0) == 4
+    assert _st(A, big, A, big, 4, 128, H.BF16, 1.0, 0) == 4     # in place too
 
 
 @cpu_only
@@ -164,6 +168,8 @@ def test_fp8_validation():
     assert _fp8(A, 128, C8, 136, S8, 4, 128, H.BF16, 1.0, 0) == 4           # codes stride % 16
     assert _fp8(A, 128, C8, 120, S8, 4, 128, H.BF16, 1.0, 0) == 4           # codes stride < n
     assert _fp8(A, 120, C8, 128, S8, 4, 128, H.BF16, 1.0, 0) == 4           # input stride < n
+    assert _fp8(A, (1 << 26) + 8, C8, 128, S8, 4, 128, H.BF16, 1.0, 0) == 4  # input stride > 2^26
+    assert _fp8(A, 128, C8, (1 << 26) + 16, S8, 4, 128, H.BF16, 1.0, 0) == 4  # codes stride > 2^26
     assert _fp8(A, 128, C8 + 8, 128, S8, 4, 128, H.BF16, 1.0, 0) == 5       # codes alignment
     assert _fp8(A, 128, C8, 128, S8 + 2, 4, 128, H.BF16, 1.0, 0) == 5       # scales alignment
     assert _fp8(A, 128, 0, 128, S8, 4, 128, H.BF16, 1.0, 0) == 1            # null codes

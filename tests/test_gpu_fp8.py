@@ -117,6 +117,28 @@ def test_fp8_strided_codes_keep_gaps(oracle, L, variant):
     assert c.ok, str(c)
 
 
+@pytest.mark.parametrize("n", [256, 4096])
+def test_fp8_large_offsets(oracle, n):
+    """Input rows 2^26 elements and code rows 2^26 bytes apart (the largest strides)."""
+    import torch
+    m, stride = 40, 1 << 26
+    say(f"fp8 large offsets n={n}: {m} rows, strides 2^26")
+    buf = torch.zeros(m * stride, dtype=torch.int16, device="cuda")
+    bits = W.random_rows(m, n, "bf16", seed=78)
+    for i in range(m):
+        buf[i * stride:i * stride + n] = torch.from_numpy(bits[i].view(np.int16)).cuda()
+    codes = torch.zeros(m * stride, dtype=torch.uint8, device="cuda")
+    scales = torch.zeros(m, dtype=torch.float32, device="cuda")
+    s = W.default_scale(n)
+    H.hadamard_transform_fp8(buf.data_ptr(), stride, codes.data_ptr(), stride, scales.data_ptr(),
+                             m, n, H.BF16, s, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    got = np.stack([codes[i * stride:i * stride + n].cpu().numpy() for i in range(m)])
+    c = compare_fp8(oracle, got, scales.cpu().numpy(), bits, "bf16", s, n)
+    del buf, codes
+    assert c.ok, str(c)
+
+
 @pytest.mark.parametrize("L", [7, 11, 14])
 def test_fp8_deterministic_and_consistent_with_transform(L, variant):
     """Repeated calls agree bit for bit; codes times scales track the 16-bit transform."""

@@ -143,11 +143,12 @@ def test_strided_rows_keep_gaps(oracle, L, dtype, variant):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-def test_large_offsets(oracle, dtype):
-    """Rows 512 MiB apart: byte offsets beyond 2^31 must address correctly."""
+@pytest.mark.parametrize("n", [256, 4096])
+def test_large_offsets(oracle, n, dtype):
+    """Rows 2^26 elements apart (the largest stride): row offsets past 2^32 bytes."""
     import torch
-    n, m, stride = 256, 5, 1 << 28
-    say(f"large offsets {dtype}: 5 rows, stride 2^28 elements")
+    m, stride = 40, 1 << 26
+    say(f"large offsets {dtype} n={n}: {m} rows, stride 2^26 elements")
     buf = torch.zeros(m * stride, dtype=torch.int16, device="cuda")
     bits = W.random_rows(m, n, dtype, seed=77)
     for i in range(m):
