@@ -10,9 +10,9 @@ What is computed (paper Sec. 2.1-2.2): for an m x n matrix of fp16/bf16 rows,
 ``y[i, j] = s * sum_k (-1)**popcount(j & k) * x[i, k]``, i.e. ``x @ H_n * s``
 with ``H_n`` the Sylvester-ordered Walsh-Hadamard matrix.  ``fwht`` follows the
 iterative radix-2 algorithm of Sec. 2.2; ``fwht_direct`` evaluates the plain
-definition one output at a time; ``fwht_fp8`` adds per-row FP8 (e4m3)
-quantization of the transformed rows (the fused transform + quantization the
-paper names as future work, Sec. 5).
+definition one output at a time; ``fwht_fp8`` and ``fwht_int8`` add per-row
+FP8 (e4m3) or symmetric INT8 quantization of the transformed rows (the fused
+transform + quantization the paper names as future work, Sec. 5).
 """
 from __future__ import annotations
 
@@ -88,6 +88,12 @@ class Oracle:
         lib.oracle_fwht_fp8.argtypes = [u16p, i64, i64, i64, ctypes.c_int, ctypes.c_double, u8p,
                                         i64, f32p]
         lib.oracle_fwht_fp8.restype = ctypes.c_int
+        i8p = ctypes.POINTER(ctypes.c_int8)
+        lib.oracle_encode_int8.argtypes = [ctypes.c_float]
+        lib.oracle_encode_int8.restype = ctypes.c_int8
+        lib.oracle_fwht_int8.argtypes = [u16p, i64, i64, i64, ctypes.c_int, ctypes.c_double, i8p,
+                                         i64, f32p]
+        lib.oracle_fwht_int8.restype = ctypes.c_int
         self.lib = lib
 
     # -- decoders ---------------------------------------------------------
@@ -178,6 +184,32 @@ class Oracle:
         if rc:
             raise ValueError("oracle_fwht_fp8 rejected its arguments")
         return codes, scales
+
+    # -- fused transform + INT8 quantization ---------------------------------
+    def encode_int8(self, values) -> np.ndarray:
+        """Round-half-to-even of float32 values to int8, saturated to [-127, 127]."""
+        v = np.asarray(values, dtype=np.float32)
+        f = self.lib.oracle_encode_int8
+        return np.fromiter((f(float(x)) for x in v.ravel()), dtype=np.int8,
+                           count=v.size).reshape(v.shape)
+
+    def fwht_int8(self, bits: np.ndarray, dtype, scale: float, n: int | None = None):
+        """Fused transform + per-row symmetric INT8 quantization: (codes (m, n) int8,
+        scales (m,) float32)."""
+        bits = np.ascontiguousarray(bits, dtype=np.uint16)
+        m, stride = bits.shape
+        n = stride if n is None else int(n)
+        codes = np.empty((m, n), dtype=np.int8)
+        scales = np.empty(m, dtype=np.float32)
+        rc = self.lib.oracle_fwht_int8(_u16(bits), stride, m, n, _dtype_code(dtype), float(scale),
+                                       _i8(codes), n, _f32(scales))
+        if rc:
+            raise ValueError("oracle_fwht_int8 rejected its arguments")
+        return codes, scales
+
+
+def _i8(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int8))
 
 
 def _u8(a):

@@ -15,8 +15,9 @@
  * The caller passes s; the paper's normalization (Sec. 2.2, the per-stage
  * division by sqrt 2 in its FWHT listing) is the special case s = 1/sqrt(n).
  *
- * Also: oracle_fwht_fp8, the transform followed by per-row FP8 (e4m3)
- * quantization (see its comment), with its own e4m3 encoder and decoder.
+ * Also: oracle_fwht_fp8 and oracle_fwht_int8, the transform followed by
+ * per-row FP8 (e4m3) or INT8 quantization (see their comments), with their own
+ * encoders and decoder.
  *
  * Two independent routes are provided for the transform itself:
  *   oracle_fwht_f64        -- the iterative radix-2 FWHT of Sec. 2.2: stage
@@ -290,6 +291,17 @@ static float max_ignoring_nan(float a, float b)
     return a > b ? a : b;
 }
 
+/* y = fp32(row * scale), and the largest |y| (NaN ignored unless all are NaN). */
+static float round_row_and_amax(const double *row, int64_t n, double scale, float *y)
+{
+    float amax = NAN;
+    for (int64_t k = 0; k < n; ++k) {
+        y[k] = (float)(row[k] * scale);
+        amax = max_ignoring_nan(amax, fabsf(y[k]));
+    }
+    return amax;
+}
+
 /*
  * Fused transform + quantization of m rows: codes (m x n bytes, row stride
  * out_stride) and scales (m floats).  Returns 0 on success, 1 on bad
@@ -307,15 +319,66 @@ int oracle_fwht_fp8(const uint16_t *in, int64_t in_stride, int64_t m, int64_t n,
         const uint16_t *src = in + i * in_stride;
         for (int64_t k = 0; k < n; ++k) row[k] = decode(src[k], dtype);
         oracle_fwht_vec_f64(row, n);
-        float amax = NAN;
-        for (int64_t k = 0; k < n; ++k) {
-            y[k] = (float)(row[k] * scale);
-            amax = max_ignoring_nan(amax, fabsf(y[k]));
-        }
+        const float amax = round_row_and_amax(row, n, scale, y);
         const float s = amax / 448.0f;
         const float inv = amax > 0.0f ? 448.0f / amax : 0.0f;
         scales[i] = s;
         for (int64_t k = 0; k < n; ++k) codes[i * out_stride + k] = oracle_encode_e4m3(y[k] * inv);
+    }
+    free(row);
+    free(y);
+    return 0;
+}
+
+/* ---- fused transform + INT8 quantization ------------------------------------
+ *
+ * The symmetric per-row INT8 counterpart of the FP8 path: the integer format
+ * that rotation-based quantization schemes target (the rotation spreads
+ * outliers so that one scale per row loses less, Sec. 1).  With amax_i as for
+ * FP8,
+ *     s_i  = amax_i / 127
+ *     q_ij = round_half_even(y_ij * inv_i),  inv_i = 127 / amax_i,
+ * an integer in [-127, 127] (|y_ij * inv_i| <= 127 up to one fp32 rounding),
+ * so that y_ij ~ q_ij * s_i.  A row whose amax is 0, +Inf or NaN gets all-zero
+ * codes: INT8 has no NaN, and 127/Inf would turn every y * inv into 0 or NaN.
+ * As for FP8 the decision is taken in fp32: y is the fp64 transform rounded
+ * once to fp32, and s, inv and the product are fp32 operations.
+ */
+
+/* Round-half-to-even of v to an integer, saturated to [-127, 127]. */
+int8_t oracle_encode_int8(float v)
+{
+    double f = floor((double)v);
+    const double r = (double)v - f;
+    if (r > 0.5 || (r == 0.5 && fmod(f, 2.0) != 0.0)) f += 1.0;
+    if (f > 127.0) f = 127.0;
+    if (f < -127.0) f = -127.0;
+    return (int8_t)f;
+}
+
+/*
+ * Fused transform + INT8 quantization of m rows: codes (m x n int8, row stride
+ * out_stride) and scales (m floats).  Returns 0 on success, 1 on bad
+ * arguments.
+ */
+int oracle_fwht_int8(const uint16_t *in, int64_t in_stride, int64_t m, int64_t n, int dtype,
+                     double scale, int8_t *codes, int64_t out_stride, float *scales)
+{
+    if (m < 0 || !is_pow2(n) || in_stride < n || out_stride < n) return 1;
+    if (dtype != ORACLE_FP16 && dtype != ORACLE_BF16) return 1;
+    double *row = (double *)malloc((size_t)n * sizeof(double));
+    float *y = (float *)malloc((size_t)n * sizeof(float));
+    if (!row || !y) { free(row); free(y); return 1; }
+    for (int64_t i = 0; i < m; ++i) {
+        const uint16_t *src = in + i * in_stride;
+        for (int64_t k = 0; k < n; ++k) row[k] = decode(src[k], dtype);
+        oracle_fwht_vec_f64(row, n);
+        const float amax = round_row_and_amax(row, n, scale, y);
+        scales[i] = amax / 127.0f;
+        const int usable = isfinite(amax) && amax > 0.0f;
+        const float inv = usable ? 127.0f / amax : 0.0f;
+        for (int64_t k = 0; k < n; ++k)
+            codes[i * out_stride + k] = usable ? oracle_encode_int8(y[k] * inv) : 0;
     }
     free(row);
     free(y);

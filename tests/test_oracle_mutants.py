@@ -2,8 +2,8 @@
 
 Each case copies ``oracle/fwht_oracle.c``, plants one mistake (a flipped
 butterfly sign, a dropped stage, a wrong pair index, an off-by-one exponent
-bias, a missing scale, an ignored stride, a wrong FP8 rounding rule or scale
-constant ...), compiles the copy on the CPU
+bias, a missing scale, an ignored stride, a wrong FP8 or INT8 rounding rule
+or scale constant ...), compiles the copy on the CPU
 into a temporary library and runs the pin battery of ``test_oracle.py``
 against it.  At least one pin must fail for every mutant.  The real oracle
 source is never modified.
@@ -16,6 +16,7 @@ import pytest
 import oracle as oracle_pkg
 import test_oracle as T
 import test_oracle_fp8 as F
+import test_oracle_int8 as I
 
 MUTANTS = [
     ("butterfly_sign", "v[j + h] = a - b;", "v[j + h] = b - a;"),
@@ -47,6 +48,15 @@ MUTANTS = [
     ("fp8_zero_guard", "amax > 0.0f ? 448.0f / amax : 0.0f", "448.0f / amax"),
     ("fp8_amax_without_abs", "amax = max_ignoring_nan(amax, fabsf(y[k]));",
      "amax = max_ignoring_nan(amax, y[k]);"),
+    # fused INT8 quantization
+    ("int8_ties_away", "if (r > 0.5 || (r == 0.5 && fmod(f, 2.0) != 0.0)) f += 1.0;",
+     "if (r >= 0.5) f += 1.0;"),
+    ("int8_truncation", "double f = floor((double)v);", "double f = trunc((double)v);"),
+    ("int8_saturation", "if (f > 127.0) f = 127.0;", "if (f > 126.0) f = 126.0;"),
+    ("int8_scale_constant", "scales[i] = amax / 127.0f;", "scales[i] = amax / 128.0f;"),
+    ("int8_inv_constant", "usable ? 127.0f / amax : 0.0f", "usable ? 128.0f / amax : 0.0f"),
+    ("int8_nonfinite_rows", "usable ? oracle_encode_int8(y[k] * inv) : 0",
+     "usable ? oracle_encode_int8(y[k] * inv) : 1"),
 ]
 
 
@@ -71,6 +81,10 @@ def _pins(o):
         lambda: F.test_hand_derived_fixtures(o),
         lambda: F.test_quantization_properties(o, "bf16", 10),
         lambda: F.test_special_rows(o),
+        lambda: I.test_encode_int8_matches_numpy_rint(o),
+        lambda: I.test_hand_derived_fixtures(o),
+        lambda: I.test_quantization_properties(o, "fp16", 7),
+        lambda: I.test_special_rows(o),
     ]
 
 
