@@ -107,7 +107,9 @@ hadacore_status hadamard_transform_strided(const void *in, int64_t in_row_stride
  *     amax_i          = max_j |y_j|   (NaN ignored unless the row is all NaN)
  *     out_scales[i]   = amax_i / 448  (fp32, correctly rounded)
  *     out_codes[i][j] = e4m3 round-to-nearest-even of y_j * (448 / amax_i)
- *                       (448/amax_i taken as 0 when amax_i is 0)
+ *                       (448/amax_i taken as 0 where it is not finite: a zero
+ *                       or NaN row, or amax_i < 448 * 2^-128, whose codes are
+ *                       then +-0)
  * so that y_j ~ decode_e4m3(out_codes[i][j]) * out_scales[i].  e4m3: 1 sign,
  * 4 exponent (bias 7) and 3 fraction bits, largest finite 448, 0x7f NaN.
  *   in              device pointer, m rows of n 16-bit values at in_row_stride
@@ -121,6 +123,23 @@ hadacore_status hadamard_transform_strided(const void *in, int64_t in_row_stride
 hadacore_status hadamard_transform_fp8(const void *in, int64_t in_row_stride, void *out_codes,
                                        int64_t out_row_stride, float *out_scales, int64_t m,
                                        int64_t n, hadacore_dtype dtype, float scale, void *stream);
+
+/*
+ * hadamard_transform_int8 -- the transform fused with symmetric per-row INT8
+ * quantization, the integer counterpart of hadamard_transform_fp8 (rotations
+ * spread outliers so that one scale per row loses less, Sec. 1).  For every
+ * row i, with y = scale * in[i] * H_n computed as above and amax_i as for FP8:
+ *     out_scales[i]   = amax_i / 127  (fp32, correctly rounded)
+ *     out_codes[i][j] = round-half-to-even of y_j * (127 / amax_i), an int8 in
+ *                       [-127, 127] (the product rounded to fp32 first)
+ * so that y_j ~ out_codes[i][j] * out_scales[i].  A row whose amax is 0, Inf or
+ * NaN, or so small that 127 / amax_i overflows fp32 (amax_i < 127 * 2^-128),
+ * gets all-zero codes; its scale is still amax_i / 127.  Arguments, layout,
+ * alignment, overlap rules, streams and errors as for hadamard_transform_fp8.
+ */
+hadacore_status hadamard_transform_int8(const void *in, int64_t in_row_stride, void *out_codes,
+                                        int64_t out_row_stride, float *out_scales, int64_t m,
+                                        int64_t n, hadacore_dtype dtype, float scale, void *stream);
 
 /*
  * hadacore_stream_copy -- copies `bytes` bytes from device pointer `src` to

@@ -94,6 +94,10 @@ class Oracle:
         lib.oracle_fwht_int8.argtypes = [u16p, i64, i64, i64, ctypes.c_int, ctypes.c_double, i8p,
                                          i64, f32p]
         lib.oracle_fwht_int8.restype = ctypes.c_int
+        lib.oracle_quantize_fp8.argtypes = [f32p, i64, i64, u8p, f32p]
+        lib.oracle_quantize_fp8.restype = ctypes.c_int
+        lib.oracle_quantize_int8.argtypes = [f32p, i64, i64, i8p, f32p]
+        lib.oracle_quantize_int8.restype = ctypes.c_int
         self.lib = lib
 
     # -- decoders ---------------------------------------------------------
@@ -205,6 +209,27 @@ class Oracle:
                                        _i8(codes), n, _f32(scales))
         if rc:
             raise ValueError("oracle_fwht_int8 rejected its arguments")
+        return codes, scales
+
+    # -- the same quantizers on plain fp32 rows (no transform) ----------------
+    def quantize_fp8(self, rows: np.ndarray):
+        """Per-row e4m3 quantization of a 2-D float32 array: (codes uint8, scales float32)."""
+        y = np.ascontiguousarray(rows, dtype=np.float32)
+        m, n = y.shape
+        codes = np.empty((m, n), dtype=np.uint8)
+        scales = np.empty(m, dtype=np.float32)
+        if self.lib.oracle_quantize_fp8(_f32(y), m, n, _u8(codes), _f32(scales)):
+            raise ValueError("oracle_quantize_fp8 rejected its arguments")
+        return codes, scales
+
+    def quantize_int8(self, rows: np.ndarray):
+        """Per-row symmetric INT8 quantization of a 2-D float32 array: (codes int8, scales)."""
+        y = np.ascontiguousarray(rows, dtype=np.float32)
+        m, n = y.shape
+        codes = np.empty((m, n), dtype=np.int8)
+        scales = np.empty(m, dtype=np.float32)
+        if self.lib.oracle_quantize_int8(_f32(y), m, n, _i8(codes), _f32(scales)):
+            raise ValueError("oracle_quantize_int8 rejected its arguments")
         return codes, scales
 
 

@@ -229,8 +229,10 @@ int oracle_fwht_direct_f64(const uint16_t *in, int64_t in_stride, int64_t n, int
  * fp32 scale per row,
  *     amax_i = max_j |y_ij|   (NaN entries ignored unless all are NaN)
  *     s_i    = amax_i / 448
- *     q_ij   = e4m3_rne(y_ij * inv_i),  inv_i = 448 / amax_i if amax_i > 0 else 0
- * so that y_ij ~ decode(q_ij) * s_i.  The quantization decision is taken in
+ *     q_ij   = e4m3_rne(y_ij * inv_i),  inv_i = 448 / amax_i if that is finite, else 0
+ * so that y_ij ~ decode(q_ij) * s_i.  inv_i = 0 covers a zero row, a NaN row
+ * and a row so small (amax_i < 448 * 2^-128) that the multiplier overflows
+ * fp32: its codes are all zero, which is within amax_i of every element.  The quantization decision is taken in
  * fp32, as the GPU kernel takes it: y is the fp64 transform rounded once to
  * fp32, and s, inv and the product are fp32 operations.
  */
@@ -291,15 +293,32 @@ static float max_ignoring_nan(float a, float b)
     return a > b ? a : b;
 }
 
-/* y = fp32(row * scale), and the largest |y| (NaN ignored unless all are NaN). */
-static float round_row_and_amax(const double *row, int64_t n, double scale, float *y)
+/* The largest |y_k| of a row of n fp32 values (NaN ignored unless all are NaN). */
+static float row_amax(const float *y, int64_t n)
 {
     float amax = NAN;
-    for (int64_t k = 0; k < n; ++k) {
-        y[k] = (float)(row[k] * scale);
-        amax = max_ignoring_nan(amax, fabsf(y[k]));
-    }
+    for (int64_t k = 0; k < n; ++k) amax = max_ignoring_nan(amax, fabsf(y[k]));
     return amax;
+}
+
+/* FP8 quantization of one row of n fp32 values: n codes and one scale. */
+static void quantize_row_fp8(const float *y, int64_t n, uint8_t *codes, float *scale)
+{
+    const float amax = row_amax(y, n);
+    const float s = amax / 448.0f;
+    const float q = 448.0f / amax;
+    const float inv = isfinite(q) ? q : 0.0f;
+    *scale = s;
+    for (int64_t k = 0; k < n; ++k) codes[k] = oracle_encode_e4m3(y[k] * inv);
+}
+
+/* Decodes row i, transforms it in fp64 and rounds y = row * scale once to fp32. */
+static void transform_row_fp32(const uint16_t *src, int64_t n, int dtype, double scale,
+                               double *row, float *y)
+{
+    for (int64_t k = 0; k < n; ++k) row[k] = decode(src[k], dtype);
+    oracle_fwht_vec_f64(row, n);
+    for (int64_t k = 0; k < n; ++k) y[k] = (float)(row[k] * scale);
 }
 
 /*
@@ -316,17 +335,23 @@ int oracle_fwht_fp8(const uint16_t *in, int64_t in_stride, int64_t m, int64_t n,
     float *y = (float *)malloc((size_t)n * sizeof(float));
     if (!row || !y) { free(row); free(y); return 1; }
     for (int64_t i = 0; i < m; ++i) {
-        const uint16_t *src = in + i * in_stride;
-        for (int64_t k = 0; k < n; ++k) row[k] = decode(src[k], dtype);
-        oracle_fwht_vec_f64(row, n);
-        const float amax = round_row_and_amax(row, n, scale, y);
-        const float s = amax / 448.0f;
-        const float inv = amax > 0.0f ? 448.0f / amax : 0.0f;
-        scales[i] = s;
-        for (int64_t k = 0; k < n; ++k) codes[i * out_stride + k] = oracle_encode_e4m3(y[k] * inv);
+        transform_row_fp32(in + i * in_stride, n, dtype, scale, row, y);
+        quantize_row_fp8(y, n, codes + i * out_stride, &scales[i]);
     }
     free(row);
     free(y);
+    return 0;
+}
+
+/*
+ * The same quantization without the transform: m rows of n fp32 values
+ * (dense) to codes (m x n) and scales (m).  The baseline of the
+ * rotation-versus-quantization comparison.  Returns 0, or 1 on bad arguments.
+ */
+int oracle_quantize_fp8(const float *y, int64_t m, int64_t n, uint8_t *codes, float *scales)
+{
+    if (m < 0 || n < 1) return 1;
+    for (int64_t i = 0; i < m; ++i) quantize_row_fp8(y + i * n, n, codes + i * n, &scales[i]);
     return 0;
 }
 
@@ -340,20 +365,34 @@ int oracle_fwht_fp8(const uint16_t *in, int64_t in_stride, int64_t m, int64_t n,
  *     q_ij = round_half_even(y_ij * inv_i),  inv_i = 127 / amax_i,
  * an integer in [-127, 127] (|y_ij * inv_i| <= 127 up to one fp32 rounding),
  * so that y_ij ~ q_ij * s_i.  A row whose amax is 0, +Inf or NaN gets all-zero
- * codes: INT8 has no NaN, and 127/Inf would turn every y * inv into 0 or NaN.
+ * codes (INT8 has no NaN, and 127/Inf would turn every y * inv into 0 or NaN),
+ * and so does a row so small (amax_i < 127 * 2^-128) that 127 / amax_i
+ * overflows fp32: zero is within amax_i of every element.
  * As for FP8 the decision is taken in fp32: y is the fp64 transform rounded
  * once to fp32, and s, inv and the product are fp32 operations.
  */
 
-/* Round-half-to-even of v to an integer, saturated to [-127, 127]. */
+/* Round-half-to-even of v to an integer, saturated to [-127, 127]; NaN -> 0. */
 int8_t oracle_encode_int8(float v)
 {
+    if (isnan(v)) return 0;
     double f = floor((double)v);
     const double r = (double)v - f;
     if (r > 0.5 || (r == 0.5 && fmod(f, 2.0) != 0.0)) f += 1.0;
     if (f > 127.0) f = 127.0;
     if (f < -127.0) f = -127.0;
     return (int8_t)f;
+}
+
+/* INT8 quantization of one row of n fp32 values: n codes and one scale. */
+static void quantize_row_int8(const float *y, int64_t n, int8_t *codes, float *scale)
+{
+    const float amax = row_amax(y, n);
+    *scale = amax / 127.0f;
+    const float q = 127.0f / amax;
+    const int usable = isfinite(amax) && isfinite(q);
+    const float inv = usable ? q : 0.0f;
+    for (int64_t k = 0; k < n; ++k) codes[k] = usable ? oracle_encode_int8(y[k] * inv) : 0;
 }
 
 /*
@@ -370,17 +409,18 @@ int oracle_fwht_int8(const uint16_t *in, int64_t in_stride, int64_t m, int64_t n
     float *y = (float *)malloc((size_t)n * sizeof(float));
     if (!row || !y) { free(row); free(y); return 1; }
     for (int64_t i = 0; i < m; ++i) {
-        const uint16_t *src = in + i * in_stride;
-        for (int64_t k = 0; k < n; ++k) row[k] = decode(src[k], dtype);
-        oracle_fwht_vec_f64(row, n);
-        const float amax = round_row_and_amax(row, n, scale, y);
-        scales[i] = amax / 127.0f;
-        const int usable = isfinite(amax) && amax > 0.0f;
-        const float inv = usable ? 127.0f / amax : 0.0f;
-        for (int64_t k = 0; k < n; ++k)
-            codes[i * out_stride + k] = usable ? oracle_encode_int8(y[k] * inv) : 0;
+        transform_row_fp32(in + i * in_stride, n, dtype, scale, row, y);
+        quantize_row_int8(y, n, codes + i * out_stride, &scales[i]);
     }
     free(row);
     free(y);
+    return 0;
+}
+
+/* INT8 quantization without the transform (see oracle_quantize_fp8). */
+int oracle_quantize_int8(const float *y, int64_t m, int64_t n, int8_t *codes, float *scales)
+{
+    if (m < 0 || n < 1) return 1;
+    for (int64_t i = 0; i < m; ++i) quantize_row_int8(y + i * n, n, codes + i * n, &scales[i]);
     return 0;
 }

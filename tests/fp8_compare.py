@@ -49,7 +49,8 @@ def compare_fp8(oracle, codes_gpu: np.ndarray, scales_gpu: np.ndarray, bits: np.
     with np.errstate(all="ignore"):
         amax = np.where(np.isnan(y32).all(axis=1), np.nan, np.nanmax(np.abs(y32), axis=1))
         amax = amax.astype(np.float32)
-        inv = np.where(amax > 0, np.float32(448.0) / amax, np.float32(0.0)).astype(np.float32)
+        q = (np.float32(448.0) / amax).astype(np.float32)
+        inv = np.where(np.isfinite(q), q, np.float32(0.0)).astype(np.float32)
         v = (y32 * inv[:, None]).astype(np.float64)
     dg = oracle.decode_e4m3(codes_gpu[:, :n])
     do = oracle.decode_e4m3(codes_o)

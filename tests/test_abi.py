@@ -152,16 +152,19 @@ def test_errors_raise_in_python():
     assert e.value.status == 2
 
 
-def _fp8(*args):
-    return H.hadamard_transform_fp8(*args, check=False)
-
-
 C8 = 1 << 34   # fake codes buffer
 S8 = 1 << 35   # fake scales buffer
+QUANTIZED = {"fp8": "hadamard_transform_fp8", "int8": "hadamard_transform_int8"}
 
 
 @cpu_only
-def test_fp8_validation():
+@pytest.mark.parametrize("fmt", sorted(QUANTIZED))
+def test_quantized_validation(fmt):
+    entry = getattr(H, QUANTIZED[fmt])
+
+    def _fp8(*args):
+        return entry(*args, check=False)
+
     ok_args = (A, 128, C8, 128, S8, 4, 128, H.BF16, 1.0, 0)
     assert _fp8(A, 128, C8, 128, S8, 4, 100, H.BF16, 1.0, 0) == 2          # size
     assert _fp8(A, 128, C8, 128, S8, 4, 128, 5, 1.0, 0) == 3                # dtype

@@ -101,6 +101,8 @@ def test_fp8_special_rows(oracle, L, dtype, variant):
     assert scales[0] == 0 and np.all((codes[0] == 0) | (codes[0] == 0x80))
     assert np.isnan(scales[1]) and np.all((codes[1] & 0x7F) == 0x7F)
     assert np.isinf(scales[2]) and np.all((codes[2] & 0x7F) == 0x7F)
+    if dtype == "bf16":   # bf16 subnormals: 448/amax overflows fp32, codes are +-0
+        assert np.all((codes[3] & 0x7F) == 0) and 0 < scales[3] < 2.0 ** -126
     c = compare_fp8(oracle, codes, scales, bits, dtype, s, n)
     assert c.ok, str(c)
 

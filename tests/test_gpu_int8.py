@@ -1,0 +1,155 @@
+"""GPU parity of the fused transform + symmetric INT8 quantization against the oracle.
+
+Criterion (tests/int8_compare.py): per-row scales within a few fp32 ulps of
+amax/127; codes equal to the oracle's, except that where the GPU's fp32
+transform can fall on the other side of a rounding boundary a code within one
+half (plus the fp32 error allowance) of the oracle's decision value is
+accepted; such mismatches must stay below 0.1%.  Rows without a usable scale
+must have all-zero codes.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from gpu_util import say, to_device, to_host
+from int8_compare import compare_int8
+from paper_2412_08832_amd import hadacore as H
+from paper_2412_08832_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+DTYPES = ["fp16", "bf16"]
+CODE = {"fp16": H.FP16, "bf16": H.BF16}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    H.library()
+    yield
+    torch.cuda.synchronize()
+
+
+@pytest.fixture(params=["auto", "valu", "mfma"])
+def variant(request, monkeypatch):
+    if request.param == "auto":
+        monkeypatch.delenv("HADACORE_VARIANT", raising=False)
+    else:
+        monkeypatch.setenv("HADACORE_VARIANT", request.param)
+    return request.param
+
+
+def _run_int8(bits: np.ndarray, dtype: str, scale: float, n: int, codes_stride: int | None = None,
+              fill: int = 0x5A):
+    import torch
+    m, in_stride = bits.shape
+    codes_stride = n if codes_stride is None else codes_stride
+    x = to_device(bits, dtype)
+    codes = torch.full((m, codes_stride), fill, dtype=torch.int8, device="cuda")
+    scales = torch.full((m,), -1.0, dtype=torch.float32, device="cuda")
+    H.hadamard_transform_int8(x.data_ptr(), in_stride, codes.data_ptr(), codes_stride,
+                              scales.data_ptr(), m, n, CODE[dtype], scale,
+                              torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    return codes.cpu().numpy(), scales.cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", range(7, 16))
+def test_int8_every_size_ragged(oracle, L, dtype, variant):
+    n = 1 << L
+    m = (1 << 20 >> L) + 3 if L <= 12 else 21
+    say(f"int8 n={n} m={m} {dtype} variant={variant}")
+    bits = W.random_rows(m, n, dtype, seed=3000 + L)
+    s = W.default_scale(n)
+    codes, scales = _run_int8(bits, dtype, s, n)
+    c = compare_int8(oracle, codes, scales, bits, dtype, s, n)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("name", ["bf16_1048576x128_inplace", "fp16_16384x4096"])
+def test_int8_outlier_workloads(oracle, name):
+    """Rotation before INT8 on the two outlier workloads (sampled rows)."""
+    w = W.WORKLOADS[name]
+    say(f"int8 {w.name}")
+    bits = W.generate(w)
+    codes, scales = _run_int8(bits, w.dtype, w.scale, w.n)
+    rows = np.unique(np.r_[0, w.m - 1, np.random.default_rng(1).integers(0, w.m, 512)])
+    c = compare_int8(oracle, codes[rows], scales[rows], np.ascontiguousarray(bits[rows]), w.dtype,
+                     w.scale, w.n)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", [7, 12, 15])
+def test_int8_special_rows(oracle, L, dtype, variant):
+    n = 1 << L
+    bits = W.random_rows(6, n, dtype, seed=9)
+    nan = 0x7E00 if dtype == "fp16" else 0x7FC0
+    inf = 0x7C00 if dtype == "fp16" else 0x7F80
+    bits[0] = 0                                   # zero row
+    bits[1, 7] = nan                              # NaN row
+    bits[2, 2] = inf                              # +-Inf row
+    rng = np.random.default_rng(2)                # subnormal-only row
+    sub = rng.integers(1, 0x3FF if dtype == "fp16" else 0x7F, n).astype(np.uint16)
+    bits[3] = sub | (rng.integers(0, 2, n).astype(np.uint16) << 15)
+    s = W.default_scale(n)
+    codes, scales = _run_int8(bits, dtype, s, n)
+    assert scales[0] == 0 and np.all(codes[0] == 0)
+    assert np.isnan(scales[1]) and np.all(codes[1] == 0)
+    assert np.isinf(scales[2]) and np.all(codes[2] == 0)
+    if dtype == "bf16":   # bf16 subnormals: 127/amax overflows fp32, codes are zero
+        assert np.all(codes[3] == 0) and 0 < scales[3] < 2.0 ** -126
+    else:                 # fp16 subnormals are ordinary small numbers here
+        assert np.abs(codes[3].astype(np.int32)).max() == 127
+    c = compare_int8(oracle, codes, scales, bits, dtype, s, n)
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("L", [7, 9, 13])
+def test_int8_strided_codes_keep_gaps(oracle, L, variant):
+    n = 1 << L
+    m = 13
+    bits = W.random_rows(m, n, "bf16", seed=L, stride=n + 40, fill_bits=0x7FC1)
+    s = W.default_scale(n)
+    codes, scales = _run_int8(bits, "bf16", s, n, codes_stride=n + 48, fill=0x5A)
+    assert (codes[:, n:] == 0x5A).all(), "codes gap was written"
+    c = compare_int8(oracle, codes[:, :n], scales, bits, "bf16", s, n)
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("L", [7, 11, 14])
+def test_int8_deterministic_and_consistent_with_transform(L, variant):
+    """Repeated calls agree bit for bit; codes times scales track the 16-bit transform."""
+    import torch
+    n = 1 << L
+    m = 64 if L <= 12 else 8
+    bits = W.random_rows(m, n, "bf16", seed=L + 5)
+    s = W.default_scale(n)
+    c1, s1 = _run_int8(bits, "bf16", s, n)
+    c2, s2 = _run_int8(bits, "bf16", s, n)
+    assert np.array_equal(c1, c2) and np.array_equal(s1, s2)
+    x = to_device(bits, "bf16")
+    y = H.transform(x, scale=s)
+    torch.cuda.synchronize()
+    y = to_host(y).astype(np.uint32) << 16
+    yv = y.view(np.float32).astype(np.float64)
+    deq = c1.astype(np.float64) * s1[:, None]
+    # half a step of the row scale, plus the bf16 rounding of the 16-bit reference
+    tol = 0.5 * s1[:, None] + 2.0 ** -8 * np.abs(yv)
+    assert np.all(np.abs(deq - yv) <= tol * (1 + 2.0 ** -10))
+
+
+def test_int8_python_wrapper():
+    import torch
+    x = torch.randn(5, 1024, device="cuda").to(torch.float16)
+    codes, scales = H.transform_int8(x)
+    torch.cuda.synchronize()
+    assert codes.dtype == torch.int8 and codes.shape == (5, 1024) and scales.shape == (5,)
+    assert int(codes.abs().max()) == 127
+    with pytest.raises(ValueError):
+        H.transform_int8(x, codes=torch.empty(5, 1024, dtype=torch.uint8, device="cuda"))

@@ -101,7 +101,14 @@ def test_special_rows(oracle):
     bits[0] = 0                      # zero row
     bits[1, 3] = 0x7FC0              # NaN -> the whole transformed row is NaN
     bits[2, 5] = 0x7F80              # +Inf -> every transformed value is +-Inf
+    tiny = np.random.default_rng(5).integers(1, 0x7F, n).astype(np.uint16)
+    bits = np.vstack([bits, tiny | (np.arange(n, dtype=np.uint16) % 2 << 15)])
+    # row 4: bf16 subnormals; 448/amax overflows fp32, so the codes are all zero
     codes, scales = oracle.fwht_fp8(bits, "bf16", W.default_scale(n))
+    amax4 = np.float32(np.abs(oracle.fwht(bits[4:5], "bf16", W.default_scale(n))
+                              .astype(np.float32)).max())
+    assert 0 < amax4 < np.float32(448.0) * np.float32(2.0 ** -128)
+    assert scales[4] == amax4 / np.float32(448.0) and ((codes[4] & 0x7F) == 0).all()  # +-0
     assert scales[0] == 0 and (codes[0] == 0).all()
     assert np.isnan(scales[1]) and np.isnan(oracle.decode_e4m3(codes[1])).all()
     assert np.isinf(scales[2]) and np.isnan(oracle.decode_e4m3(codes[2])).all()
@@ -114,3 +121,11 @@ def test_power_of_two_scale_equivariance(oracle):
     c2, s2 = oracle.fwht_fp8(bits, "fp16", 0.125)
     assert np.array_equal(c1, c2)
     assert np.array_equal(s2, 2 * s1)
+
+
+def test_plain_row_quantizer_on_fixture_rows(oracle):
+    """Without the transform the same quantizer maps the fixtures' y rows to their codes."""
+    for c in json.loads(GOLDEN.read_text())["cases"]:
+        codes, scales = oracle.quantize_fp8(np.array([c["y"]], dtype=np.float32))
+        assert list(codes[0]) == c["codes"], c
+        assert scales[0] == np.float32(c["scale_out"]), (scales[0], c)

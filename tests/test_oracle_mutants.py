@@ -45,16 +45,18 @@ MUTANTS = [
     ("e4m3_subnormal_spacing", "spacing = ldexp(1.0, -9);", "spacing = ldexp(1.0, -10);"),
     ("e4m3_decode_bias", "expo - 10", "expo - 11"),
     ("fp8_scale_constant", "const float s = amax / 448.0f;", "const float s = amax / 480.0f;"),
-    ("fp8_zero_guard", "amax > 0.0f ? 448.0f / amax : 0.0f", "448.0f / amax"),
-    ("fp8_amax_without_abs", "amax = max_ignoring_nan(amax, fabsf(y[k]));",
+    ("fp8_multiplier_guard", "const float inv = isfinite(q) ? q : 0.0f;", "const float inv = q;"),
+    ("amax_without_abs", "amax = max_ignoring_nan(amax, fabsf(y[k]));",
      "amax = max_ignoring_nan(amax, y[k]);"),
     # fused INT8 quantization
     ("int8_ties_away", "if (r > 0.5 || (r == 0.5 && fmod(f, 2.0) != 0.0)) f += 1.0;",
      "if (r >= 0.5) f += 1.0;"),
     ("int8_truncation", "double f = floor((double)v);", "double f = trunc((double)v);"),
     ("int8_saturation", "if (f > 127.0) f = 127.0;", "if (f > 126.0) f = 126.0;"),
-    ("int8_scale_constant", "scales[i] = amax / 127.0f;", "scales[i] = amax / 128.0f;"),
-    ("int8_inv_constant", "usable ? 127.0f / amax : 0.0f", "usable ? 128.0f / amax : 0.0f"),
+    ("int8_scale_constant", "*scale = amax / 127.0f;", "*scale = amax / 128.0f;"),
+    ("int8_inv_constant", "const float q = 127.0f / amax;", "const float q = 128.0f / amax;"),
+    ("int8_multiplier_overflow", "const int usable = isfinite(amax) && isfinite(q);",
+     "const int usable = isfinite(amax) && amax > 0.0f;"),
     ("int8_nonfinite_rows", "usable ? oracle_encode_int8(y[k] * inv) : 0",
      "usable ? oracle_encode_int8(y[k] * inv) : 1"),
 ]
