@@ -47,6 +47,8 @@ def parse_args(argv=None):
     p.add_argument("--sweep", metavar="FILE", help="also time every workload, one JSON line each")
     p.add_argument("--fp8", action="store_true",
                    help="time the fused transform + e4m3 quantization instead of the transform")
+    p.add_argument("--int8", action="store_true",
+                   help="time the fused transform + int8 quantization instead of the transform")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="target duration of the CPU oracle baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -127,29 +129,30 @@ class Device:
 
 
 def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0,
-                  fp8: bool = False) -> dict:
-    """Time one workload: the transform (16-bit out, in place or not) or, with fp8,
-    the fused transform + per-row e4m3 quantization (codes + scales out)."""
+                  quant: str | None = None) -> dict:
+    """Time one workload: the transform (16-bit out, in place or not) or, with quant
+    "fp8" / "int8", the fused transform + per-row quantization (codes + scales out)."""
     from paper_2412_08832_amd import workloads as W
     H, torch = d.H, d.torch
     bits = W.generate(w)
     code = H.FP16 if w.dtype == "fp16" else H.BF16
     nbytes = w.m * w.n * 2
-    per_set = nbytes + (w.m * w.n + 4 * w.m if fp8 else (0 if w.inplace else nbytes))
+    per_set = nbytes + (w.m * w.n + 4 * w.m if quant else (0 if w.inplace else nbytes))
     nbuf = max(2, math.ceil(ROTATING_BYTES / per_set))
     first = d.upload(bits, w.dtype)
     del bits
     ins = [first] + [first.clone() for _ in range(nbuf - 1)]
     s = d.stream.cuda_stream
-    if fp8:
+    if quant:
+        entry = {"fp8": H.hadamard_transform_fp8, "int8": H.hadamard_transform_int8}[quant]
         codes = [torch.empty((w.m, w.n), dtype=torch.uint8, device=d.dev) for _ in range(nbuf)]
         scales = [torch.empty((w.m,), dtype=torch.float32, device=d.dev) for _ in range(nbuf)]
         calls = [
-            (lambda i=i: H.hadamard_transform_fp8(ins[i].data_ptr(), w.n, codes[i].data_ptr(), w.n,
-                                                  scales[i].data_ptr(), w.m, w.n, code, w.scale, s))
+            (lambda i=i: entry(ins[i].data_ptr(), w.n, codes[i].data_ptr(), w.n,
+                               scales[i].data_ptr(), w.m, w.n, code, w.scale, s))
             for i in range(nbuf)
         ]
-        alg_bytes = w.m * w.n * 3 + 4 * w.m          # 16-bit read, e4m3 write, one scale per row
+        alg_bytes = w.m * w.n * 3 + 4 * w.m          # 16-bit read, 1-byte code write, row scales
         outs = codes
     else:
         outs = ins if w.inplace else [torch.empty_like(first) for _ in range(nbuf)]
@@ -164,7 +167,7 @@ def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0
     gbs = alg_bytes / per_launch / 1e9
 
     # device copy of the same element bytes: the achievable-bandwidth reference
-    dsts = [torch.empty_like(first) for _ in range(nbuf)] if (w.inplace or fp8) else outs
+    dsts = [torch.empty_like(first) for _ in range(nbuf)] if (w.inplace or quant) else outs
     copies = [
         (lambda i=i: H.hadacore_stream_copy(ins[i].data_ptr(), dsts[i].data_ptr(), nbytes, s))
         for i in range(nbuf)
@@ -174,17 +177,17 @@ def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0
     del ins, outs, dsts, first, calls
     torch.cuda.empty_cache()
     return {
-        "workload": w.name + ("_fp8" if fp8 else ""), "dtype": w.dtype, "m": w.m, "n": w.n,
-        "inplace": w.inplace and not fp8, "fp8": fp8,
+        "workload": w.name + (f"_{quant}" if quant else ""), "dtype": w.dtype, "m": w.m,
+        "n": w.n, "inplace": w.inplace and not quant, "output": quant or w.dtype,
         "steps": steps, "rotating_buffers": nbuf, "ms_per_step": per_launch * 1e3,
         "elements_per_s": w.m * w.n / per_launch, "gbs": gbs, "frac_hbm_peak": gbs / HBM_PEAK_GBS,
         "copy_gbs": copy_gbs, "frac_of_copy": gbs / copy_gbs, "alg_bytes_per_launch": alg_bytes,
     }
 
 
-def cpu_baseline(w, target_seconds: float, fp8: bool = False) -> dict:
+def cpu_baseline(w, target_seconds: float, quant: str | None = None) -> dict:
     """The fp64 oracle on the host cores, timed on a bounded row sample of the workload
-    (with fp8, the oracle's fused transform + e4m3 quantization, which runs on one thread)."""
+    (with quant, the oracle's fused transform + quantization, which runs on one thread)."""
     import numpy as np
     import oracle
     from paper_2412_08832_amd import workloads as W
@@ -192,16 +195,18 @@ def cpu_baseline(w, target_seconds: float, fp8: bool = False) -> dict:
         cores = len(os.sched_getaffinity(0))
     except AttributeError:
         cores = os.cpu_count() or 1
-    cores = 1 if fp8 else max(1, min(cores, 16))
+    cores = 1 if quant else max(1, min(cores, 16))
     orc = oracle.get()
 
     def run(b):
-        if fp8:
+        if quant == "fp8":
             orc.fwht_fp8(b, w.dtype, w.scale)
+        elif quant == "int8":
+            orc.fwht_int8(b, w.dtype, w.scale)
         else:
             orc.fwht(b, w.dtype, w.scale, nthreads=cores)
 
-    probe_rows = max(1, min(w.m, (1 << 20) // w.n // (16 if fp8 else 1)))
+    probe_rows = max(1, min(w.m, (1 << 20) // w.n // (16 if quant else 1)))
     bits = W.generate(w, rows=probe_rows)
     t0 = time.perf_counter()
     run(bits)
@@ -229,8 +234,8 @@ def cpu_baseline(w, target_seconds: float, fp8: bool = False) -> dict:
         "value": passes * rows * w.n / sec, "unit": "elements/s", "cores": cores, "kind": "oracle",
         "sample": f"{passes} pass(es) over the first {rows} of {w.m} rows ({rows * w.n} "
                   f"elements each), {sec:.1f} s, "
-                  + ("fp64 iterative FWHT + e4m3 quantization in C on 1 thread, " if fp8 else
-                     f"fp64 iterative FWHT in C on {cores} threads, ") + cpu,
+                  + (f"fp64 iterative FWHT + {quant} quantization in C on 1 thread, " if quant
+                     else f"fp64 iterative FWHT in C on {cores} threads, ") + cpu,
     }
 
 
@@ -240,9 +245,12 @@ def main(argv=None) -> int:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); rows are "
               "independent, so N GPUs would each run this kernel on m/N rows.", file=sys.stderr)
         return 2
+    if args.fp8 and args.int8:
+        raise SystemExit("--fp8 and --int8 are exclusive")
+    quant = "fp8" if args.fp8 else ("int8" if args.int8 else None)
     w = workload_by_name(args.workload)
     d = Device()
-    r = time_workload(d, w, args.steps, args.warmup, fp8=args.fp8)
+    r = time_workload(d, w, args.steps, args.warmup, quant=quant)
     digest = source_digest()
     traffic = measured_traffic(r["workload"], digest)
     line = {
@@ -260,7 +268,9 @@ def main(argv=None) -> int:
         "data": "synthetic",
         "config": {
             "workload": r["workload"], "m": w.m, "n": w.n, "io_dtype": w.dtype,
-            "inplace": r["inplace"], "output": "e4m3 codes + fp32 row scales" if args.fp8 else w.dtype,
+            "inplace": r["inplace"],
+            "output": f"{'e4m3' if quant == 'fp8' else 'int8'} codes + fp32 row scales" if quant
+            else w.dtype,
             "scale": w.scale, "rotating_buffers": r["rotating_buffers"],
             "achieved_gbs": r["gbs"], "frac_hbm_peak": r["frac_hbm_peak"],
             "copy_gbs": r["copy_gbs"], "frac_of_copy": r["frac_of_copy"],
@@ -276,19 +286,19 @@ def main(argv=None) -> int:
         for inplace in (True, False):
             for dt in ("fp16", "bf16"):
                 points += [W.sweep_point(k, dt, inplace) for k in range(7, 16)]
-        fp8_points = [W.sweep_point(k, "bf16", False) for k in range(7, 16)]
-        fp8_points += [W.WORKLOADS["bf16_1048576x128_inplace"], W.WORKLOADS["fp16_16384x4096"]]
-        jobs = [(p, False) for p in points] + [(p, True) for p in fp8_points]
+        q_points = [W.sweep_point(k, "bf16", False) for k in range(7, 16)]
+        q_points += [W.WORKLOADS["bf16_1048576x128_inplace"], W.WORKLOADS["fp16_16384x4096"]]
+        jobs = [(p, None) for p in points] + [(p, q) for q in ("fp8", "int8") for p in q_points]
         with open(args.sweep, "w") as f:
-            for p, fp8 in jobs:
-                pr = time_workload(d, p, args.steps, args.warmup, min_warm_s=0.03, fp8=fp8)
+            for p, q in jobs:
+                pr = time_workload(d, p, args.steps, args.warmup, min_warm_s=0.03, quant=q)
                 f.write(json.dumps(pr) + "\n")
                 f.flush()
                 print(f"[sweep] {pr['workload']}: {pr['gbs']:.0f} GB/s ({100 * pr['frac_hbm_peak']:.1f}% "
                       f"of peak, {100 * pr['frac_of_copy']:.1f}% of copy)", file=sys.stderr,
                       flush=True)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, fp8=args.fp8)
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, quant=quant)
     print(json.dumps(line), flush=True)
     return 0
 

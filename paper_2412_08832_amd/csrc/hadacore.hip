@@ -434,16 +434,22 @@ struct ScaleArgs {
 
 // ---- fused FP8 epilogue ------------------------------------------------------------
 //
-// The transform followed by per-row quantization to OCP FP8 e4m3 (the fused
-// transform + quantization the paper names as future work, Sec. 5):
-//   amax = max_j |y_j| (NaN ignored unless the row is all NaN), s = amax/448,
-//   code_j = e4m3_rne(y_j * inv) with inv = 448/amax (0 for a zero row),
-// the divisions correctly rounded in fp32.  y ~ decode(code) * s.
+// The transform followed by per-row quantization (the fused transform +
+// quantization the paper names as future work, Sec. 5), with
+// amax = max_j |y_j| (NaN ignored unless the row is all NaN) and Q = 448 (OCP
+// FP8 e4m3) or 127 (symmetric INT8):
+//   s = amax / Q,  code_j = round(y_j * inv),  inv = Q / amax,
+// the divisions and the product correctly rounded in fp32.  FP8 rounds to
+// e4m3 (to nearest even) and takes inv = 0 where Q / amax is not finite (a
+// zero or NaN row, or amax < Q * 2^-128); INT8 rounds half to even to an
+// integer in [-127, 127] and gives those rows, and rows whose amax is Inf,
+// all-zero codes.  y ~ code * s.
 
 constexpr int kStore16 = 0;  // 16-bit output in the input dtype
 constexpr int kFp8 = 1;      // e4m3 codes + one fp32 scale per row
+constexpr int kInt8 = 2;     // int8 codes + one fp32 scale per row
 
-struct Fp8Out {
+struct QuantOut {
   uint8_t *codes;
   int64_t stride;  // bytes between rows of codes
   float *scales;   // one per row
@@ -506,6 +512,25 @@ __device__ __forceinline__ u2 to_e4m3x8(const float *v, float mul) {
   return u2{(uint32_t)lo, (uint32_t)hi};
 }
 
+// 8 values times `mul` to 8 int8 codes, round half to even, AND-ed with `keep`
+// (0 clears the codes of a row without a usable scale).  q + 1.5 * 2^23 rounds
+// q (|q| <= 127) to an integer in the low mantissa bits, whose low byte is the
+// two's-complement code.  The product is rounded before the addition, as in
+// the definition, so contraction into an fma is switched off.
+__device__ __forceinline__ u2 to_int8x8(const float *v, float mul, uint32_t keep) {
+#pragma clang fp contract(off)
+  uint32_t b[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) b[j] = __builtin_bit_cast(uint32_t, v[j] * mul + 12582912.0f);
+  // byte j of the result is the low byte of b[j]
+  const uint32_t p01 = __builtin_amdgcn_perm(b[1], b[0], 0x0C0C0400u);
+  const uint32_t p23 = __builtin_amdgcn_perm(b[3], b[2], 0x0C0C0400u);
+  const uint32_t p45 = __builtin_amdgcn_perm(b[5], b[4], 0x0C0C0400u);
+  const uint32_t p67 = __builtin_amdgcn_perm(b[7], b[6], 0x0C0C0400u);
+  return u2{__builtin_amdgcn_perm(p23, p01, 0x05040100u) & keep,
+            __builtin_amdgcn_perm(p67, p45, 0x05040100u) & keep};
+}
+
 template <bool NT>
 __device__ __forceinline__ void gstore8_at(void *base, uint32_t off, u2 v) {
   u2 *q = reinterpret_cast<u2 *>(static_cast<char *>(base) + off);
@@ -519,24 +544,37 @@ __device__ __forceinline__ void gstore8_at(void *base, uint32_t off, u2 v) {
 // Row scale and quantization multiplier of a lane, given the largest |register|
 // of its row.  The multiplier includes the twist sign (and, for kMfma, the part
 // of the scale the front end left out).  Both correctly rounded quotients come
-// from one division: even lanes form 448 / amax, odd lanes amax / 448, and the
+// from one division: even lanes form Q / amax, odd lanes amax / Q, and the
 // pair swaps them (lanes 2i and 2i+1 always hold the same row).  Requires all
 // lanes active.
-template <int FRONT>
-struct Fp8Quant {
-  float scale;  // amax / 448
-  float mul;    // (twist sign) * (kMfma: post) * 448 / amax, 0 for a zero row
-  __device__ __forceinline__ Fp8Quant(float reg_amax, bool tw, float post, int lane) {
+template <int FRONT, int EPI>
+struct RowQuant {
+  float scale;    // amax / Q
+  float mul;      // (twist sign) * (kMfma: post) * Q / amax, 0 where Q / amax is not finite
+  uint32_t keep;  // kInt8: all ones, or 0 to clear the codes of a row without a usable scale
+  __device__ __forceinline__ RowQuant(float reg_amax, bool tw, float post, int lane) {
+    constexpr float Q = EPI == kFp8 ? 448.0f : 127.0f;
     const float mag = FRONT == kMfma ? fabsf(post) : 1.0f;
     const float amax = reg_amax * mag;
     const bool odd = (lane & 1) != 0;
-    const float q = (odd ? amax : 448.0f) / (odd ? 448.0f : amax);
+    const float q = (odd ? amax : Q) / (odd ? Q : amax);
     const float qp = __builtin_bit_cast(
         float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, q), 0xB1, 0xF, 0xF, true));
-    const float inv = amax > 0.0f ? (odd ? qp : q) : 0.0f;
+    const float inv_raw = odd ? qp : q;  // Q / amax
+    const bool finite_inv = inv_raw < __builtin_inff();  // false for Inf and NaN
+    const bool usable = EPI == kFp8 ? finite_inv : (finite_inv && amax < __builtin_inff());
+    const float inv = usable ? inv_raw : 0.0f;
     scale = odd ? q : qp;
     const float to_true = FRONT == kMfma ? (tw ? -post : post) : (tw ? -1.0f : 1.0f);
     mul = to_true * inv;
+    keep = usable ? 0xFFFFFFFFu : 0u;
+  }
+  __device__ __forceinline__ u2 codes(const float *v) const {
+    if constexpr (EPI == kFp8) {
+      return to_e4m3x8(v, mul);
+    } else {
+      return to_int8x8(v, mul, keep);
+    }
   }
 };
 
@@ -553,7 +591,7 @@ struct Fp8Quant {
 template <int DT, int L, int C, int T, int WPB, bool NT, int FRONT, int EPI>
 __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
     const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, int64_t m,
-    ScaleArgs sc, Fp8Out fp8) {
+    ScaleArgs sc, QuantOut qo) {
   constexpr int kTile = 512 * C;
   static_assert((1 << L) <= kTile, "row does not fit a wave tile");
   constexpr int kRows = kTile >> L;
@@ -566,7 +604,7 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
 
   const int lf_load = lane_field_load<FRONT, L>(lane);
   const int lf = lane_field<FRONT, L>(lane);
-  const int64_t out_pitch = EPI == kStore16 ? out_stride * 2 : fp8.stride;  // bytes per row
+  const int64_t out_pitch = EPI == kStore16 ? out_stride * 2 : qo.stride;  // bytes per row
   int ld_row[C], st_row[C];
   uint32_t ld_off[C], st_off[C];
 #pragma unroll
@@ -585,8 +623,8 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
 
   const char *src = reinterpret_cast<const char *>(in) + row0 * in_stride * 2;
   char *dst = EPI == kStore16 ? reinterpret_cast<char *>(out) + row0 * out_pitch
-                              : reinterpret_cast<char *>(fp8.codes) + row0 * out_pitch;
-  float *scales = EPI == kStore16 ? nullptr : fp8.scales + row0;
+                              : reinterpret_cast<char *>(qo.codes) + row0 * out_pitch;
+  float *scales = EPI == kStore16 ? nullptr : qo.scales + row0;
   auto rows_in_tile = [&](int64_t r0) { return (int)(m - r0 < kRows ? m - r0 : kRows); };
   auto load_tile = [&](const char *base, int valid, u4(&raw)[C]) {
 #pragma unroll
@@ -650,13 +688,13 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
 #pragma unroll
       for (int k = 0; k < C; ++k) {
         if ((k & kChunkRow) != 0) continue;  // same row as chunk k & ~kChunkRow
-        const Fp8Quant<FRONT> qz(lane_max<row_lane_mask<FRONT, L>()>(a[k], lane), tw, sc.post,
-                                 lane);
+        const RowQuant<FRONT, EPI> qz(lane_max<row_lane_mask<FRONT, L>()>(a[k], lane), tw,
+                                      sc.post, lane);
 #pragma unroll
         for (int j = 0; j < C; ++j) {
           if ((j & ~kChunkRow) != k) continue;
           if (kRows == 1 || st_row[j] < cur_valid) {
-            gstore8_at<NT>(dst, st_off[j], to_e4m3x8(&v[j * 8], qz.mul));
+            gstore8_at<NT>(dst, st_off[j], qz.codes(&v[j * 8]));
           }
         }
         if ((lane & row_lane_mask<FRONT, L>()) == 0 && (kRows == 1 || st_row[k] < cur_valid)) {
@@ -681,7 +719,7 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
 template <int DT, int L, int C, int HALVES, bool NT, int FRONT, int EPI>
 __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
     const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc,
-    Fp8Out fp8) {
+    QuantOut qo) {
   constexpr int n = 1 << L;
   constexpr int NW = n / (512 * C);
   static_assert(NW >= 2 && NW <= C, "wave bits must fit the chunk bits");
@@ -759,14 +797,14 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
     a = wave_max[0];
 #pragma unroll
     for (int i = 1; i < NW; ++i) a = fmaxf(a, wave_max[i]);
-    const Fp8Quant<FRONT> qz(a, twisted<FRONT, L>(lane), sc.post, lane);
-    uint8_t *codes = fp8.codes + row * fp8.stride;
+    const RowQuant<FRONT, EPI> qz(a, twisted<FRONT, L>(lane), sc.post, lane);
+    uint8_t *codes = qo.codes + row * qo.stride;
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const int W = (k % NW) * C + (k / NW) * NW + w;
-      gstore8_at<NT>(codes, (uint32_t)((W * kWave + lf) * 8), to_e4m3x8(&v[k * 8], qz.mul));
+      gstore8_at<NT>(codes, (uint32_t)((W * kWave + lf) * 8), qz.codes(&v[k * 8]));
     }
-    if (threadIdx.x == 0) fp8.scales[row] = qz.scale;
+    if (threadIdx.x == 0) qo.scales[row] = qz.scale;
   }
 }
 
@@ -801,18 +839,18 @@ ScaleArgs split_scale(float scale, int dtype) {
 // (wave kernel); HALVES: LDS exchange passes (block kernel); FRONT: kValu / kMfma.
 template <int DT, int L, int C, int T, int WPB, int HALVES, int FRONT, int EPI = kStore16>
 hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
-                      int64_t m, const ScaleArgs &sc, hipStream_t stream, Fp8Out fp8 = {}) {
+                      int64_t m, const ScaleArgs &sc, hipStream_t stream, QuantOut qo = {}) {
   if constexpr ((1 << L) <= 512 * C) {
     constexpr int64_t rows_per_wave = (int64_t)T * ((512 * C) >> L);
     const int64_t waves = (m + rows_per_wave - 1) / rows_per_wave;
     const int64_t blocks = (waves + WPB - 1) / WPB;
     hipLaunchKernelGGL((fwht_wave_kernel<DT, L, C, T, WPB, true, FRONT, EPI>),
                        dim3((uint32_t)blocks), dim3(kWave * WPB), 0, stream, in, in_stride, out,
-                       out_stride, m, sc, fp8);
+                       out_stride, m, sc, qo);
   } else {
     hipLaunchKernelGGL((fwht_block_kernel<DT, L, C, HALVES, true, FRONT, EPI>), dim3((uint32_t)m),
                        dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out, out_stride, sc,
-                       fp8);
+                       qo);
   }
   return hipGetLastError();
 }
@@ -830,10 +868,10 @@ struct Cfg {
 // workgroup, exchange passes and front end, interleaved so that every
 // candidate sees the same clock state).  16-bit output: the smallest per-wave
 // footprint that holds a row wins up to n = 2048, and from n = 4096 a row
-// spreads over the waves of a workgroup with one LDS exchange.  FP8 output
-// has more arithmetic per byte, so small rows amortize the per-wave setup and
-// the row reduction over two tiles or chunks per wave, and n = 4096 stays in
-// one wave.
+// spreads over the waves of a workgroup with one LDS exchange.  Quantized
+// output (FP8, INT8) has more arithmetic per byte, so small rows amortize the
+// per-wave setup and the row reduction over two tiles or chunks per wave, and
+// n = 4096 stays in one wave.
 template <int L, int EPI, int FRONT>
 constexpr Cfg config() {
   if constexpr (EPI == kStore16) {
@@ -859,44 +897,44 @@ constexpr Cfg config() {
 }
 
 // Front end used unless HADACORE_VARIANT forces one: the matrix cores from
-// n = 2048 for 16-bit output, everywhere for FP8 output.
+// n = 2048 for 16-bit output, everywhere for quantized output.
 template <int L, int EPI>
 constexpr int default_front() {
-  return (EPI == kFp8 || L >= 11) ? kMfma : kValu;
+  return (EPI != kStore16 || L >= 11) ? kMfma : kValu;
 }
 
 template <int DT, int L, int EPI, int FRONT>
 hipError_t launch_front(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
-                        int64_t m, const ScaleArgs &sc, hipStream_t stream, Fp8Out fp8) {
+                        int64_t m, const ScaleArgs &sc, hipStream_t stream, QuantOut qo) {
   constexpr Cfg c = config<L, EPI, FRONT>();
   return launch_cfg<DT, L, c.C, c.T, c.WPB, c.HALVES, FRONT, EPI>(in, in_stride, out, out_stride,
-                                                                  m, sc, stream, fp8);
+                                                                  m, sc, stream, qo);
 }
 
 // `front` < 0 takes the default; kValu / kMfma force one front end.
 template <int DT, int L, int EPI>
 hipError_t launch(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
-                  int64_t m, const ScaleArgs &sc, int front, hipStream_t stream, Fp8Out fp8) {
+                  int64_t m, const ScaleArgs &sc, int front, hipStream_t stream, QuantOut qo) {
   const int f = front < 0 ? default_front<L, EPI>() : front;
   return f == kMfma
-             ? launch_front<DT, L, EPI, kMfma>(in, in_stride, out, out_stride, m, sc, stream, fp8)
-             : launch_front<DT, L, EPI, kValu>(in, in_stride, out, out_stride, m, sc, stream, fp8);
+             ? launch_front<DT, L, EPI, kMfma>(in, in_stride, out, out_stride, m, sc, stream, qo)
+             : launch_front<DT, L, EPI, kValu>(in, in_stride, out, out_stride, m, sc, stream, qo);
 }
 
 template <int DT, int EPI = kStore16>
 hipError_t launch_dt(int L, const uint16_t *in, int64_t in_stride, uint16_t *out,
                      int64_t out_stride, int64_t m, const ScaleArgs &sc, int front,
-                     hipStream_t stream, Fp8Out fp8 = {}) {
+                     hipStream_t stream, QuantOut qo = {}) {
   switch (L) {
-    case 7: return launch<DT, 7, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
-    case 8: return launch<DT, 8, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
-    case 9: return launch<DT, 9, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
-    case 10: return launch<DT, 10, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
-    case 11: return launch<DT, 11, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
-    case 12: return launch<DT, 12, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
-    case 13: return launch<DT, 13, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
-    case 14: return launch<DT, 14, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
-    case 15: return launch<DT, 15, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, fp8);
+    case 7: return launch<DT, 7, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 8: return launch<DT, 8, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 9: return launch<DT, 9, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 10: return launch<DT, 10, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 11: return launch<DT, 11, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 12: return launch<DT, 12, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 13: return launch<DT, 13, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 14: return launch<DT, 14, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 15: return launch<DT, 15, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1008,10 +1046,14 @@ extern "C" hadacore_status hadamard_transform(const void *in, void *out, int64_t
   return hadamard_transform_strided(in, n, out, n, m, n, dtype, scale, stream);
 }
 
-extern "C" hadacore_status hadamard_transform_fp8(const void *in, int64_t in_row_stride,
-                                                  void *out_codes, int64_t out_row_stride,
-                                                  float *out_scales, int64_t m, int64_t n,
-                                                  hadacore_dtype dtype, float scale, void *stream) {
+namespace hadacore {
+namespace {
+
+// Validation and launch shared by the quantizing entry points.
+template <int EPI>
+hadacore_status transform_quantized(const void *in, int64_t in_row_stride, void *out_codes,
+                                    int64_t out_row_stride, float *out_scales, int64_t m,
+                                    int64_t n, hadacore_dtype dtype, float scale, void *stream) {
   if (m < 0) return HADACORE_ERROR_INVALID_VALUE;
   const int L = log2_exact(n);
   if (L < 7 || L > 15) return HADACORE_ERROR_INVALID_SIZE;
@@ -1045,13 +1087,32 @@ extern "C" hadacore_status hadamard_transform_fp8(const void *in, int64_t in_row
   const uint16_t *src = static_cast<const uint16_t *>(in);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const ScaleArgs sc = split_scale(scale, dtype);
-  const Fp8Out fp8{static_cast<uint8_t *>(out_codes), out_row_stride, out_scales};
+  const QuantOut qo{static_cast<uint8_t *>(out_codes), out_row_stride, out_scales};
   const int front = front_override();
   const hipError_t err =
       dtype == HADACORE_FP16
-          ? launch_dt<HADACORE_FP16, kFp8>(L, src, in_row_stride, nullptr, 0, m, sc, front, s, fp8)
-          : launch_dt<HADACORE_BF16, kFp8>(L, src, in_row_stride, nullptr, 0, m, sc, front, s, fp8);
+          ? launch_dt<HADACORE_FP16, EPI>(L, src, in_row_stride, nullptr, 0, m, sc, front, s, qo)
+          : launch_dt<HADACORE_BF16, EPI>(L, src, in_row_stride, nullptr, 0, m, sc, front, s, qo);
   return err == hipSuccess ? HADACORE_SUCCESS : HADACORE_ERROR_LAUNCH;
+}
+
+}  // namespace
+}  // namespace hadacore
+
+extern "C" hadacore_status hadamard_transform_fp8(const void *in, int64_t in_row_stride,
+                                                  void *out_codes, int64_t out_row_stride,
+                                                  float *out_scales, int64_t m, int64_t n,
+                                                  hadacore_dtype dtype, float scale, void *stream) {
+  return transform_quantized<kFp8>(in, in_row_stride, out_codes, out_row_stride, out_scales, m, n,
+                                   dtype, scale, stream);
+}
+
+extern "C" hadacore_status hadamard_transform_int8(const void *in, int64_t in_row_stride,
+                                                   void *out_codes, int64_t out_row_stride,
+                                                   float *out_scales, int64_t m, int64_t n,
+                                                   hadacore_dtype dtype, float scale, void *stream) {
+  return transform_quantized<kInt8>(in, in_row_stride, out_codes, out_row_stride, out_scales, m,
+                                    n, dtype, scale, stream);
 }
 
 extern "C" hadacore_status hadacore_stream_copy(const void *src, void *dst, int64_t bytes,

@@ -6,9 +6,9 @@ directory; if it is missing, every call raises (there is no fallback).
 
 The raw entry points take device addresses as integers and keep the C names:
 ``hadamard_transform``, ``hadamard_transform_strided``, ``hadamard_transform_fp8``,
-``hadacore_stream_copy``, ``hadacore_status_string``, ``hadacore_version``.
-``transform`` and ``transform_fp8`` are convenience wrappers for 2-D torch
-tensors on a ROCm device.
+``hadamard_transform_int8``, ``hadacore_stream_copy``, ``hadacore_status_string``,
+``hadacore_version``.  ``transform``, ``transform_fp8`` and ``transform_int8`` are
+convenience wrappers for 2-D torch tensors on a ROCm device.
 """
 from __future__ import annotations
 
@@ -27,7 +27,8 @@ STATUS_NAMES = {
     8: "UNSUPPORTED_DEVICE", 9: "TOO_LARGE",
 }
 EXPORTS = ("hadamard_transform", "hadamard_transform_strided", "hadamard_transform_fp8",
-           "hadacore_stream_copy", "hadacore_status_string", "hadacore_version")
+           "hadamard_transform_int8", "hadacore_stream_copy", "hadacore_status_string",
+           "hadacore_version")
 
 
 class HadacoreError(RuntimeError):
@@ -55,6 +56,8 @@ def library() -> ctypes.CDLL:
         lib.hadamard_transform_strided.restype = i32
         lib.hadamard_transform_fp8.argtypes = [vp, i64, vp, i64, vp, i64, i64, i32, f32, vp]
         lib.hadamard_transform_fp8.restype = i32
+        lib.hadamard_transform_int8.argtypes = [vp, i64, vp, i64, vp, i64, i64, i32, f32, vp]
+        lib.hadamard_transform_int8.restype = i32
         lib.hadacore_stream_copy.argtypes = [vp, vp, i64, vp]
         lib.hadacore_stream_copy.restype = i32
         lib.hadacore_status_string.argtypes = [i32]
@@ -95,6 +98,16 @@ def hadamard_transform_fp8(in_ptr: int, in_row_stride: int, codes_ptr: int, code
                                           scales_ptr, m, n, dtype, scale, stream)
     if check:
         _check(st, "hadamard_transform_fp8")
+    return st
+
+
+def hadamard_transform_int8(in_ptr: int, in_row_stride: int, codes_ptr: int,
+                            codes_row_stride: int, scales_ptr: int, m: int, n: int, dtype: int,
+                            scale: float, stream: int = 0, check: bool = True) -> int:
+    st = library().hadamard_transform_int8(in_ptr, in_row_stride, codes_ptr, codes_row_stride,
+                                           scales_ptr, m, n, dtype, scale, stream)
+    if check:
+        _check(st, "hadamard_transform_int8")
     return st
 
 
@@ -158,25 +171,19 @@ def transform(x, out=None, scale: float | None = None, n: int | None = None, str
     return out
 
 
-def transform_fp8(x, codes=None, scales=None, scale: float | None = None, stream=None):
-    """Fused transform + per-row e4m3 quantization of a 2-D float16/bfloat16 tensor.
-
-    Returns (codes, scales): codes is a (m, n) torch.uint8 tensor of e4m3 bit
-    patterns (view it as torch.float8_e4m3fn to decode) and scales a (m,)
-    float32 tensor, so that x @ H_n * scale ~ codes.float() * scales[:, None].
-    """
+def _transform_quantized(x, codes, scales, scale, stream, entry, codes_dtype):
     import torch
     if x.dim() != 2 or not x.is_cuda or x.stride(1) != 1:
         raise ValueError("expected a 2-D ROCm tensor with contiguous rows")
     code = _dtype_code(x)
     m, n = x.shape
     if codes is None:
-        codes = torch.empty((m, n), dtype=torch.uint8, device=x.device)
+        codes = torch.empty((m, n), dtype=codes_dtype, device=x.device)
     if scales is None:
         scales = torch.empty((m,), dtype=torch.float32, device=x.device)
-    if codes.dtype != torch.uint8 or codes.dim() != 2 or codes.stride(1) != 1 \
+    if codes.dtype != codes_dtype or codes.dim() != 2 or codes.stride(1) != 1 \
             or tuple(codes.shape) != (m, n):
-        raise ValueError("codes must be a (m, n) uint8 tensor with contiguous rows")
+        raise ValueError(f"codes must be a (m, n) {codes_dtype} tensor with contiguous rows")
     if scales.dtype != torch.float32 or scales.numel() != m or not scales.is_contiguous():
         raise ValueError("scales must be a contiguous float32 tensor of m elements")
     if scale is None:
@@ -188,6 +195,28 @@ def transform_fp8(x, codes=None, scales=None, scale: float | None = None, stream
     in_stride = x.stride(0) if m > 1 else n
     codes_stride = codes.stride(0) if m > 1 else ((n + 15) // 16) * 16
     with torch.cuda.device(x.device):
-        hadamard_transform_fp8(x.data_ptr(), in_stride, codes.data_ptr(), codes_stride,
-                               scales.data_ptr(), m, n, code, scale, stream)
+        entry(x.data_ptr(), in_stride, codes.data_ptr(), codes_stride, scales.data_ptr(), m, n,
+              code, scale, stream)
     return codes, scales
+
+
+def transform_fp8(x, codes=None, scales=None, scale: float | None = None, stream=None):
+    """Fused transform + per-row e4m3 quantization of a 2-D float16/bfloat16 tensor.
+
+    Returns (codes, scales): codes is a (m, n) torch.uint8 tensor of e4m3 bit
+    patterns (view it as torch.float8_e4m3fn to decode) and scales a (m,)
+    float32 tensor, so that x @ H_n * scale ~ codes.float() * scales[:, None].
+    """
+    import torch
+    return _transform_quantized(x, codes, scales, scale, stream, hadamard_transform_fp8,
+                                torch.uint8)
+
+
+def transform_int8(x, codes=None, scales=None, scale: float | None = None, stream=None):
+    """Fused transform + symmetric per-row INT8 quantization of a 2-D float16/bfloat16
+    tensor.  Returns (codes, scales): a (m, n) torch.int8 tensor and a (m,) float32
+    tensor, so that x @ H_n * scale ~ codes.float() * scales[:, None].
+    """
+    import torch
+    return _transform_quantized(x, codes, scales, scale, stream, hadamard_transform_int8,
+                                torch.int8)
