@@ -286,7 +286,9 @@ def main(argv=None) -> int:
         for inplace in (True, False):
             for dt in ("fp16", "bf16"):
                 points += [W.sweep_point(k, dt, inplace) for k in range(7, 16)]
-        q_points = [W.sweep_point(k, "bf16", False) for k in range(7, 16)]
+        # sizes below the paper's range: bf16, both modes
+        points += [W.sweep_point(k, "bf16", ip) for ip in (True, False) for k in range(0, 7)]
+        q_points = [W.sweep_point(k, "bf16", False) for k in range(0, 16)]
         q_points += [W.WORKLOADS["bf16_1048576x128_inplace"], W.WORKLOADS["fp16_16384x4096"]]
         jobs = [(p, None) for p in points] + [(p, q) for q in ("fp8", "int8") for p in q_points]
         with open(args.sweep, "w") as f:

@@ -10,8 +10,10 @@
  * i.e. each row is multiplied on the right by the Sylvester-ordered
  * Walsh-Hadamard matrix H_n (natural order, +-1 entries), and by `scale`.
  * The normalized transform of the paper is scale = 1/sqrt(n); H_n is never
- * stored.  n is a power of two from 2^7 to 2^15 (Sec. 2.3-2.4 and Sec. 3.2
- * bound the sizes at 2^15).  In-place operation (Appendix B) is supported.
+ * stored.  n is a power of two from 1 to 2^15: the paper's sizes are 2^7 to
+ * 2^15 (Sec. 2.3-2.4 and Sec. 3.2 bound them at 2^15); the smaller ones are
+ * supported as well (n = 1 is the identity times `scale`).  In-place operation
+ * (Appendix B) is supported.
  *
  * Numerics: inputs are scaled before any addition -- by `scale`, or by its
  * power-of-two part with the remaining factor (in [1, 2)) applied at the end --
@@ -25,8 +27,10 @@
  * never allocates, frees or retains them.  Rows are contiguous (element
  * stride 1) and start every `row_stride` elements; elements between n and the
  * row stride are neither read nor written.  Row strides are at most 2^26
- * elements (bytes for FP8 codes), which keeps every offset inside a group of
- * rows handled by one wave below 2^32 bytes.
+ * elements (bytes for quantized codes), which keeps every offset inside a
+ * group of rows handled by one wave below 2^32 bytes, and multiples of
+ * min(n, 8) elements (codes: min(n, 16) bytes), so that every row starts on a
+ * boundary of its access width.
  *
  * Streams: work is enqueued asynchronously on `stream` (a hipStream_t; NULL
  * means the default stream) and the call returns without synchronizing.
@@ -36,9 +40,10 @@
  * Kernels: per transform size the library picks one of two front ends for the
  * first stages, both giving results within fp32 rounding of each other: fp32
  * VALU butterflies, or one radix-32 step on the matrix cores (MFMA) applied
- * directly to the 16-bit inputs.  The environment variable HADACORE_VARIANT
- * set to "valu" or "mfma" forces one of them (testing and tuning; read on
- * every call); unset keeps the measured per-size choice.
+ * directly to the 16-bit inputs (n >= 128 only).  The environment variable
+ * HADACORE_VARIANT set to "valu" or "mfma" forces one of them for n >= 128
+ * (testing and tuning; read on every call); unset keeps the measured per-size
+ * choice.
  *
  * Errors: arguments are validated synchronously before anything is enqueued;
  * on error nothing is enqueued and a nonzero status is returned.  No call
@@ -63,9 +68,9 @@ typedef int32_t hadacore_dtype;
 typedef int32_t hadacore_status;
 #define HADACORE_SUCCESS 0
 #define HADACORE_ERROR_INVALID_VALUE 1      /* m < 0, null pointer with m > 0, non-finite scale */
-#define HADACORE_ERROR_INVALID_SIZE 2       /* n not a power of two in [128, 32768] */
+#define HADACORE_ERROR_INVALID_SIZE 2       /* n not a power of two in [1, 32768] */
 #define HADACORE_ERROR_INVALID_DTYPE 3      /* dtype not HADACORE_FP16 / HADACORE_BF16 */
-#define HADACORE_ERROR_INVALID_STRIDE 4     /* row stride < n, > 2^26, or not a multiple of 8 */
+#define HADACORE_ERROR_INVALID_STRIDE 4     /* row stride < n, > 2^26, or not a multiple of min(n, 8) */
 #define HADACORE_ERROR_MISALIGNED 5         /* in or out not 16-byte aligned */
 #define HADACORE_ERROR_OVERLAP 6            /* in/out overlap without being the same layout */
 #define HADACORE_ERROR_LAUNCH 7             /* the HIP runtime rejected the kernel launch */
@@ -80,7 +85,7 @@ typedef int32_t hadacore_status;
  *          selects in-place operation, any other overlap is rejected
  *   m      number of rows, >= 0; m == 0 returns HADACORE_SUCCESS and enqueues
  *          nothing (pointers may then be NULL)
- *   n      transform length, a power of two in [128, 32768]
+ *   n      transform length, a power of two in [1, 32768]
  *   dtype  HADACORE_FP16 or HADACORE_BF16 (input and output share it)
  *   scale  finite fp32 multiplier; 1/sqrt(n) gives the orthonormal transform
  *   stream hipStream_t to enqueue on (NULL = default stream)
@@ -92,7 +97,7 @@ hadacore_status hadamard_transform(const void *in, void *out, int64_t m, int64_t
 /*
  * hadamard_transform_strided -- as hadamard_transform, with row i of the input
  * at in + i*in_row_stride and row i of the output at out + i*out_row_stride
- * (strides in elements, each >= n, <= 2^26 and a multiple of 8).  In-place operation
+ * (strides in elements, each >= n, <= 2^26 and a multiple of min(n, 8)).  In-place operation
  * requires in == out and in_row_stride == out_row_stride.
  */
 hadacore_status hadamard_transform_strided(const void *in, int64_t in_row_stride, void *out,
@@ -113,9 +118,10 @@ hadacore_status hadamard_transform_strided(const void *in, int64_t in_row_stride
  * so that y_j ~ decode_e4m3(out_codes[i][j]) * out_scales[i].  e4m3: 1 sign,
  * 4 exponent (bias 7) and 3 fraction bits, largest finite 448, 0x7f NaN.
  *   in              device pointer, m rows of n 16-bit values at in_row_stride
- *                   elements (>= n, <= 2^26, multiple of 8), 16-byte aligned
+ *                   elements (>= n, <= 2^26, multiple of min(n, 8)), 16-byte
+ *                   aligned
  *   out_codes       device pointer, m rows of n bytes at out_row_stride bytes
- *                   (>= n, <= 2^26, multiple of 16), 16-byte aligned
+ *                   (>= n, <= 2^26, multiple of min(n, 16)), 16-byte aligned
  *   out_scales      device pointer to m floats, 4-byte aligned
  * The three ranges must not overlap (OVERLAP otherwise).  Other arguments,
  * streams, ownership and errors as for hadamard_transform.

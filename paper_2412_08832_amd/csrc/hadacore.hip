@@ -1,9 +1,11 @@
 // hadacore.hip -- batched normalized Walsh-Hadamard transform for gfx950.
 //
 // Computes out[i][j] = scale * sum_k (-1)^popcount(j & k) * in[i][k] for
-// 16-bit rows of length n = 2^L, 7 <= L <= 15 (HadaCore, arXiv 2412.08832:
-// the transform of Sec. 2.1-2.2, sizes of Sec. 3.2, in place per Appendix B,
-// fp16 and bf16 per Appendix C).
+// 16-bit rows of length n = 2^L, 0 <= L <= 15 (HadaCore, arXiv 2412.08832:
+// the transform of Sec. 2.1-2.2, sizes of Sec. 3.2 -- 2^7 to 2^15 -- plus the
+// smaller ones, in place per Appendix B, fp16 and bf16 per Appendix C).
+// Rows of n <= 8 are one per thread (fwht_row_kernel); the tile structure
+// below applies from n = 16.
 //
 // Structure of one launch.  The radix-2 stages of the fast transform (Sec.
 // 2.2) act on the bits of the element index, one stage per bit, and stages on
@@ -560,13 +562,20 @@ struct RowQuant {
     const float q = (odd ? amax : Q) / (odd ? Q : amax);
     const float qp = __builtin_bit_cast(
         float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, q), 0xB1, 0xF, 0xF, true));
-    const float inv_raw = odd ? qp : q;  // Q / amax
+    scale = odd ? q : qp;
+    finish(amax, odd ? qp : q, FRONT == kMfma ? (tw ? -post : post) : (tw ? -1.0f : 1.0f));
+  }
+  // One thread holds the whole row (no twist, no residual scale): both
+  // quotients computed directly.
+  __device__ __forceinline__ explicit RowQuant(float amax) {
+    constexpr float Q = EPI == kFp8 ? 448.0f : 127.0f;
+    scale = amax / Q;
+    finish(amax, Q / amax, 1.0f);
+  }
+  __device__ __forceinline__ void finish(float amax, float inv_raw, float to_true) {
     const bool finite_inv = inv_raw < __builtin_inff();  // false for Inf and NaN
     const bool usable = EPI == kFp8 ? finite_inv : (finite_inv && amax < __builtin_inff());
-    const float inv = usable ? inv_raw : 0.0f;
-    scale = odd ? q : qp;
-    const float to_true = FRONT == kMfma ? (tw ? -post : post) : (tw ? -1.0f : 1.0f);
-    mul = to_true * inv;
+    mul = to_true * (usable ? inv_raw : 0.0f);
     keep = usable ? 0xFFFFFFFFu : 0u;
   }
   __device__ __forceinline__ u2 codes(const float *v) const {
@@ -808,6 +817,119 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   }
 }
 
+// n <= 8: one row per thread.  A row is n consecutive 16-bit values, 2n bytes
+// aligned to 2n by the stride rules, loaded and stored as one access; its
+// L stages are register butterflies after scaling, and quantized outputs
+// reduce, divide and convert inside the thread.  Consecutive threads take
+// consecutive rows, so dense rows are read and written contiguously.
+template <int N>
+struct RowBits;
+template <>
+struct RowBits<1> {
+  typedef uint16_t T;
+};
+template <>
+struct RowBits<2> {
+  typedef uint32_t T;
+};
+template <>
+struct RowBits<4> {
+  typedef u2 T;
+};
+template <>
+struct RowBits<8> {
+  typedef u4 T;
+};
+
+template <int N>
+__device__ __forceinline__ void unpack16(typename RowBits<N>::T r, uint32_t (&h)[N]) {
+  if constexpr (N == 1) {
+    h[0] = r;
+  } else if constexpr (N == 2) {
+    h[0] = r & 0xFFFFu;
+    h[1] = r >> 16;
+  } else {
+#pragma unroll
+    for (int q = 0; q < N / 2; ++q) {
+      h[2 * q] = r[q] & 0xFFFFu;
+      h[2 * q + 1] = r[q] >> 16;
+    }
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ float widen1(uint32_t h) {
+  if constexpr (DT == HADACORE_FP16) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+  } else {
+    return __builtin_bit_cast(float, h << 16);
+  }
+}
+
+template <int DT, int L, bool NT, int EPI>
+__global__ __launch_bounds__(256) void fwht_row_kernel(const uint16_t *in, int64_t in_stride,
+                                                       uint16_t *out, int64_t out_stride,
+                                                       int64_t m, ScaleArgs sc, QuantOut qo) {
+  constexpr int N = 1 << L;
+  typedef typename RowBits<N>::T T;
+  const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (row >= m) return;
+  const T *src = reinterpret_cast<const T *>(in + row * in_stride);
+  const T raw = NT ? __builtin_nontemporal_load(src) : *src;
+  uint32_t h[N];
+  unpack16<N>(raw, h);
+  float v[N > 8 ? N : 8];
+#pragma unroll
+  for (int j = 0; j < N; ++j) v[j] = widen1<DT>(h[j]) * sc.scale;
+#pragma unroll
+  for (int b = 0; b < L; ++b) {
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      if ((j & (1 << b)) == 0) {
+        const float a = v[j], c = v[j + (1 << b)];
+        v[j] = a + c;
+        v[j + (1 << b)] = a - c;
+      }
+    }
+  }
+  if constexpr (EPI == kStore16) {
+    T r;
+    if constexpr (N == 1) {
+      r = (T)(narrow<DT>(v[0], 0.0f, 0u) & 0xFFFFu);
+    } else if constexpr (N == 2) {
+      r = narrow<DT>(v[0], v[1], 0u);
+    } else {
+#pragma unroll
+      for (int q = 0; q < N / 2; ++q) r[q] = narrow<DT>(v[2 * q], v[2 * q + 1], 0u);
+    }
+    T *dst = reinterpret_cast<T *>(out + row * out_stride);
+    if constexpr (NT) {
+      __builtin_nontemporal_store(r, dst);
+    } else {
+      *dst = r;
+    }
+  } else {
+    float amax = fabsf(v[0]);
+#pragma unroll
+    for (int j = 1; j < N; ++j) amax = fmaxf(amax, fabsf(v[j]));
+#pragma unroll
+    for (int j = N; j < 8; ++j) v[j] = 0.0f;
+    const RowQuant<kValu, EPI> qz(amax);
+    const u2 c = qz.codes(v);
+    uint8_t *dst = qo.codes + row * qo.stride;
+    if constexpr (N == 8) {
+      gstore8_at<NT>(dst, 0, c);
+    } else if constexpr (N == 4) {
+      *reinterpret_cast<uint32_t *>(dst) = c.x;
+    } else if constexpr (N == 2) {
+      *reinterpret_cast<uint16_t *>(dst) = (uint16_t)c.x;
+    } else {
+      *dst = (uint8_t)c.x;
+    }
+    qo.scales[row] = qz.scale;
+  }
+}
+
 // 16-byte streaming copy, one access per thread, the bandwidth reference for
 // the transform.
 __global__ __launch_bounds__(256) void stream_copy_kernel(const uint16_t *src, uint16_t *dst,
@@ -840,7 +962,10 @@ ScaleArgs split_scale(float scale, int dtype) {
 template <int DT, int L, int C, int T, int WPB, int HALVES, int FRONT, int EPI = kStore16>
 hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
                       int64_t m, const ScaleArgs &sc, hipStream_t stream, QuantOut qo = {}) {
-  if constexpr ((1 << L) <= 512 * C) {
+  if constexpr (L <= 3) {
+    hipLaunchKernelGGL((fwht_row_kernel<DT, L, true, EPI>), dim3((uint32_t)((m + 255) / 256)),
+                       dim3(256), 0, stream, in, in_stride, out, out_stride, m, sc, qo);
+  } else if constexpr ((1 << L) <= 512 * C) {
     constexpr int64_t rows_per_wave = (int64_t)T * ((512 * C) >> L);
     const int64_t waves = (m + rows_per_wave - 1) / rows_per_wave;
     const int64_t blocks = (waves + WPB - 1) / WPB;
@@ -874,7 +999,9 @@ struct Cfg {
 // n = 4096 stays in one wave.
 template <int L, int EPI, int FRONT>
 constexpr Cfg config() {
-  if constexpr (EPI == kStore16) {
+  if constexpr (L <= 6) {
+    return {1, 1, 1, 1};  // n <= 8: one row per thread; n = 16..64: one tile per wave
+  } else if constexpr (EPI == kStore16) {
     if constexpr (L <= 9) return {1, 1, 1, 1};
     if constexpr (L == 10) return {2, 1, 1, 1};
     if constexpr (L == 11 || L == 12) return {4, 1, 1, 1};
@@ -897,10 +1024,12 @@ constexpr Cfg config() {
 }
 
 // Front end used unless HADACORE_VARIANT forces one: the matrix cores from
-// n = 2048 for 16-bit output, everywhere for quantized output.
+// n = 2048 for 16-bit output, everywhere from n = 128 for quantized output.
+// Below n = 128 there is only the VALU front (the radix-32 step needs 16 vectors
+// of 32 elements per wave with four lanes per vector row group).
 template <int L, int EPI>
 constexpr int default_front() {
-  return (EPI != kStore16 || L >= 11) ? kMfma : kValu;
+  return L >= 7 && (EPI != kStore16 || L >= 11) ? kMfma : kValu;
 }
 
 template <int DT, int L, int EPI, int FRONT>
@@ -915,10 +1044,15 @@ hipError_t launch_front(const uint16_t *in, int64_t in_stride, uint16_t *out, in
 template <int DT, int L, int EPI>
 hipError_t launch(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
                   int64_t m, const ScaleArgs &sc, int front, hipStream_t stream, QuantOut qo) {
-  const int f = front < 0 ? default_front<L, EPI>() : front;
-  return f == kMfma
-             ? launch_front<DT, L, EPI, kMfma>(in, in_stride, out, out_stride, m, sc, stream, qo)
-             : launch_front<DT, L, EPI, kValu>(in, in_stride, out, out_stride, m, sc, stream, qo);
+  if constexpr (L < 7) {
+    (void)front;
+    return launch_front<DT, L, EPI, kValu>(in, in_stride, out, out_stride, m, sc, stream, qo);
+  } else {
+    const int f = front < 0 ? default_front<L, EPI>() : front;
+    return f == kMfma
+               ? launch_front<DT, L, EPI, kMfma>(in, in_stride, out, out_stride, m, sc, stream, qo)
+               : launch_front<DT, L, EPI, kValu>(in, in_stride, out, out_stride, m, sc, stream, qo);
+  }
 }
 
 template <int DT, int EPI = kStore16>
@@ -926,6 +1060,13 @@ hipError_t launch_dt(int L, const uint16_t *in, int64_t in_stride, uint16_t *out
                      int64_t out_stride, int64_t m, const ScaleArgs &sc, int front,
                      hipStream_t stream, QuantOut qo = {}) {
   switch (L) {
+    case 0: return launch<DT, 0, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 1: return launch<DT, 1, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 2: return launch<DT, 2, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 3: return launch<DT, 3, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 4: return launch<DT, 4, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 5: return launch<DT, 5, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 6: return launch<DT, 6, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
     case 7: return launch<DT, 7, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
     case 8: return launch<DT, 8, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
     case 9: return launch<DT, 9, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
@@ -991,11 +1132,12 @@ hadacore_status validate(const void *in, int64_t in_row_stride, const void *out,
                          float scale, int *L_out) {
   if (m < 0) return HADACORE_ERROR_INVALID_VALUE;
   const int L = log2_exact(n);
-  if (L < 7 || L > 15) return HADACORE_ERROR_INVALID_SIZE;
+  if (L < 0 || L > 15) return HADACORE_ERROR_INVALID_SIZE;
   if (dtype != HADACORE_FP16 && dtype != HADACORE_BF16) return HADACORE_ERROR_INVALID_DTYPE;
   if (!isfinite(scale)) return HADACORE_ERROR_INVALID_VALUE;
-  if (in_row_stride < n || out_row_stride < n || (in_row_stride % 8) != 0 ||
-      (out_row_stride % 8) != 0 || in_row_stride > kMaxStride || out_row_stride > kMaxStride)
+  const int64_t align = n < 8 ? n : 8;  // rows start on 2*min(n, 8)-byte boundaries
+  if (in_row_stride < n || out_row_stride < n || (in_row_stride % align) != 0 ||
+      (out_row_stride % align) != 0 || in_row_stride > kMaxStride || out_row_stride > kMaxStride)
     return HADACORE_ERROR_INVALID_STRIDE;
   *L_out = L;
   if (m == 0) return HADACORE_SUCCESS;
@@ -1056,11 +1198,13 @@ hadacore_status transform_quantized(const void *in, int64_t in_row_stride, void 
                                     int64_t n, hadacore_dtype dtype, float scale, void *stream) {
   if (m < 0) return HADACORE_ERROR_INVALID_VALUE;
   const int L = log2_exact(n);
-  if (L < 7 || L > 15) return HADACORE_ERROR_INVALID_SIZE;
+  if (L < 0 || L > 15) return HADACORE_ERROR_INVALID_SIZE;
   if (dtype != HADACORE_FP16 && dtype != HADACORE_BF16) return HADACORE_ERROR_INVALID_DTYPE;
   if (!isfinite(scale)) return HADACORE_ERROR_INVALID_VALUE;
-  if (in_row_stride < n || (in_row_stride % 8) != 0 || out_row_stride < n ||
-      (out_row_stride % 16) != 0 || in_row_stride > kMaxStride || out_row_stride > kMaxStride)
+  // input rows start on 2*min(n, 8)-byte boundaries, code rows on min(n, 16)
+  if (in_row_stride < n || (in_row_stride % (n < 8 ? n : 8)) != 0 || out_row_stride < n ||
+      (out_row_stride % (n < 16 ? n : 16)) != 0 || in_row_stride > kMaxStride ||
+      out_row_stride > kMaxStride)
     return HADACORE_ERROR_INVALID_STRIDE;
   if (m == 0) return HADACORE_SUCCESS;
   if (in == nullptr || out_codes == nullptr || out_scales == nullptr)
@@ -1138,10 +1282,10 @@ extern "C" const char *hadacore_status_string(hadacore_status status) {
   switch (status) {
     case HADACORE_SUCCESS: return "success";
     case HADACORE_ERROR_INVALID_VALUE: return "invalid value (m < 0, null pointer or non-finite scale)";
-    case HADACORE_ERROR_INVALID_SIZE: return "invalid size (n must be a power of two in [128, 32768])";
+    case HADACORE_ERROR_INVALID_SIZE: return "invalid size (n must be a power of two in [1, 32768])";
     case HADACORE_ERROR_INVALID_DTYPE: return "invalid dtype (expected HADACORE_FP16 or HADACORE_BF16)";
     case HADACORE_ERROR_INVALID_STRIDE:
-      return "invalid row stride (must be >= n, a multiple of 8 (16 for FP8 codes) and <= 2^26)";
+      return "invalid row stride (>= n, <= 2^26, a multiple of min(n, 8) (codes: min(n, 16)))";
     case HADACORE_ERROR_MISALIGNED: return "misaligned pointer (16-byte alignment required)";
     case HADACORE_ERROR_OVERLAP: return "input and output overlap without being the same layout";
     case HADACORE_ERROR_LAUNCH: return "kernel launch failed";

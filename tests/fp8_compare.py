@@ -5,7 +5,7 @@ y32 being the exact transform rounded once to fp32.  A GPU code must decode to
 the oracle's code, or -- where the GPU's fp32 transform (whose error is a small
 multiple of 2^-24 of the row's magnitudes) can land on the other side of a
 rounding boundary -- to a value within half an e4m3 step plus that error of v.
-Scales must agree within a few fp32 ulps.  -0 equals +0.
+Scales must agree within a few fp32 ulps (two subnormal steps for scales below 2^-126).  -0 equals +0.
 """
 from __future__ import annotations
 
@@ -15,6 +15,9 @@ import numpy as np
 
 REL_FP32_SLACK = 2.0 ** -17      # fp32 transform error allowance, relative to the row maximum
 SCALE_RTOL = 2.0 ** -19          # a few fp32 ulps
+# plus two fp32 subnormal steps: a row scale below 2^-126 has fewer significant
+# bits, and the fp32 transform's error in amax can move its last one
+SCALE_ATOL = 2.0 * 2.0 ** -149
 MAX_MISMATCH_FRACTION = 1e-3
 
 
@@ -63,7 +66,8 @@ def compare_fp8(oracle, codes_gpu: np.ndarray, scales_gpu: np.ndarray, bits: np.
     so = scales_o.astype(np.float64)
     same_class = (np.isnan(sg) == np.isnan(so)) & (np.isinf(sg) == np.isinf(so))
     with np.errstate(all="ignore"):
-        close = np.where(np.isfinite(so), np.abs(sg - so) <= SCALE_RTOL * np.abs(so), sg == so)
+        close = np.where(np.isfinite(so), np.abs(sg - so) <= SCALE_RTOL * np.abs(so) + SCALE_ATOL,
+                         sg == so)
     close = close | (np.isnan(sg) & np.isnan(so))
     return Fp8Comparison(count=int(dg.size), mismatches=int(np.count_nonzero(~exact)),
                          invalid=int(np.count_nonzero(~valid)),

@@ -7,7 +7,7 @@ multiple of 2^-24 of the row's magnitudes) can land on the other side of a
 rounding boundary -- lie within one half plus that error of v.  Rows without a
 usable scale (amax 0, Inf or NaN, or 127/amax overflowing fp32) must have
 all-zero codes.  Scales must agree
-within a few fp32 ulps.
+within a few fp32 ulps (two subnormal steps for scales below 2^-126).
 """
 from __future__ import annotations
 
@@ -17,6 +17,9 @@ import numpy as np
 
 REL_FP32_SLACK = 2.0 ** -17      # fp32 transform error allowance, relative to the row maximum
 SCALE_RTOL = 2.0 ** -19          # a few fp32 ulps
+# plus two fp32 subnormal steps: a row scale below 2^-126 has fewer significant
+# bits, and the fp32 transform's error in amax can move its last one
+SCALE_ATOL = 2.0 * 2.0 ** -149
 MAX_MISMATCH_FRACTION = 1e-3
 
 
@@ -58,7 +61,8 @@ def compare_int8(oracle, codes_gpu: np.ndarray, scales_gpu: np.ndarray, bits: np
     so = scales_o.astype(np.float64)
     same_class = (np.isnan(sg) == np.isnan(so)) & (np.isinf(sg) == np.isinf(so))
     with np.errstate(all="ignore"):
-        close = np.where(np.isfinite(so), np.abs(sg - so) <= SCALE_RTOL * np.abs(so), sg == so)
+        close = np.where(np.isfinite(so), np.abs(sg - so) <= SCALE_RTOL * np.abs(so) + SCALE_ATOL,
+                         sg == so)
     close = close | (np.isnan(sg) & np.isnan(so))
     return Int8Comparison(count=int(cg.size), mismatches=int(np.count_nonzero(~exact)),
                           invalid=int(np.count_nonzero(~valid)),

@@ -71,7 +71,7 @@ def _st(*args):
 
 
 @cpu_only
-@pytest.mark.parametrize("n", [0, 1, 2, 64, 100, 127, 129, 3 * 1024, 65536, -128])
+@pytest.mark.parametrize("n", [0, 3, 6, 100, 127, 129, 3 * 1024, 65536, -128])
 def test_invalid_size(n):
     assert _st(A, 65536, B, 65536, 4, n, H.FP16, 1.0, 0) == 2
 
@@ -96,6 +96,9 @@ def test_invalid_strides():
     assert _st(A, 120, B, 128, 4, 128, H.FP16, 1.0, 0) == 4     # in stride < n
     assert _st(A, 128, B, 64, 4, 128, H.FP16, 1.0, 0) == 4      # out stride < n
     assert _st(A, 132, B, 128, 4, 128, H.FP16, 1.0, 0) == 4     # not a multiple of 8
+    assert _st(A, 20, B, 16, 4, 16, H.FP16, 1.0, 0) == 4        # n = 16: multiple of 8
+    assert _st(A, 6, B, 4, 4, 4, H.FP16, 1.0, 0) == 4           # n = 4: multiple of 4
+    assert _st(A, 2, B, 3, 4, 2, H.BF16, 1.0, 0) == 4           # n = 2: multiple of 2
     big = (1 << 26) + 8                                          # above the 2^26 stride limit
     assert _st(A, big, B, 128, 4, 128, H.FP16, 1.0, 0) == 4
     assert _st(A, 128, B, big, 4, 128, H.BF16, 1.0, 0) == 4
@@ -169,6 +172,8 @@ def test_quantized_validation(fmt):
     assert _fp8(A, 128, C8, 128, S8, 4, 100, H.BF16, 1.0, 0) == 2          # size
     assert _fp8(A, 128, C8, 128, S8, 4, 128, 5, 1.0, 0) == 3                # dtype
     assert _fp8(A, 128, C8, 136, S8, 4, 128, H.BF16, 1.0, 0) == 4           # codes stride % 16
+    assert _fp8(A, 8, C8, 12, S8, 4, 8, H.BF16, 1.0, 0) == 4                # n = 8: codes % 8
+    assert _fp8(A, 6, C8, 4, S8, 4, 4, H.BF16, 1.0, 0) == 4                 # n = 4: input % 4
     assert _fp8(A, 128, C8, 120, S8, 4, 128, H.BF16, 1.0, 0) == 4           # codes stride < n
     assert _fp8(A, 120, C8, 128, S8, 4, 128, H.BF16, 1.0, 0) == 4           # input stride < n
     assert _fp8(A, (1 << 26) + 8, C8, 128, S8, 4, 128, H.BF16, 1.0, 0) == 4  # input stride > 2^26

@@ -61,13 +61,13 @@ def _run(bits: np.ndarray, dtype: str, scale: float, n: int, inplace: bool,
 
 def _ragged_rows(L: int) -> int:
     # n <= 4096 spans many workgroups and leaves a ragged tail (multi-row tiles for
-    # n <= 256); larger n run one row per workgroup
+    # n <= 256, one row per thread for n <= 8); larger n run one row per workgroup
     return (1 << 21 >> L) + 3 if L <= 12 else 37
 
 
 @pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", range(7, 16))
+@pytest.mark.parametrize("L", range(0, 16))
 def test_every_size_ragged(oracle, L, dtype, inplace, variant):
     n = 1 << L
     m = _ragged_rows(L)
@@ -92,7 +92,7 @@ def test_configs_full_size(oracle, name):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", range(7, 16))
+@pytest.mark.parametrize("L", [1, 4, 6] + list(range(7, 16)))
 def test_sweep_full_size_sampled(oracle, L, dtype):
     w = W.sweep_point(L, dtype, inplace=True)
     say(f"sweep {w.name} (sampled rows)")
@@ -106,7 +106,7 @@ def test_sweep_full_size_sampled(oracle, L, dtype):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [7, 8, 11, 12, 13, 15])
+@pytest.mark.parametrize("L", [0, 2, 5, 7, 8, 11, 12, 13, 15])
 def test_single_row(oracle, L, dtype, variant):
     n = 1 << L
     bits = W.random_rows(1, n, dtype, seed=7 + L)
@@ -125,7 +125,7 @@ def test_zero_rows_leaves_output_untouched():
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [7, 9, 12, 14])
+@pytest.mark.parametrize("L", [1, 3, 5, 7, 9, 12, 14])
 def test_strided_rows_keep_gaps(oracle, L, dtype, variant):
     n = 1 << L
     m = 19
@@ -165,14 +165,14 @@ def test_large_offsets(oracle, n, dtype):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [7, 10, 13, 15])
+@pytest.mark.parametrize("L", [0, 1, 3, 5, 7, 10, 13, 15])
 def test_special_vectors(L, dtype, variant):
     n = 1 << L
     one = W.round_to_bits(np.array([1.0], np.float32), dtype)[0]
     rows = np.zeros((4, n), np.uint16)
     rows[0, 0] = one                       # delta -> all ones
     rows[1, :] = one                       # ones -> n e_0
-    k = n // 2 + 5                         # a Walsh row -> n e_k
+    k = (n // 2 + 5) % n                   # a Walsh row -> n e_k
     parity = np.array([bin(k & j).count("1") & 1 for j in range(n)])
     rows[2] = W.round_to_bits(np.where(parity == 1, -1.0, 1.0).astype(np.float32), dtype)
     # row 3 stays zero
@@ -189,14 +189,14 @@ def test_special_vectors(L, dtype, variant):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [7, 12, 15])
+@pytest.mark.parametrize("L", [1, 2, 5, 7, 12, 15])
 def test_nonfinite_and_subnormal_inputs(oracle, L, dtype, variant):
     n = 1 << L
     bits = W.random_rows(6, n, dtype, seed=3)
     nan = 0x7E00 if dtype == "fp16" else 0x7FC0
     inf = 0x7C00 if dtype == "fp16" else 0x7F80
     bits[0, n // 3] = nan
-    bits[1, 5] = inf
+    bits[1, 5 % n] = inf
     bits[2, 1] = inf
     bits[2, n - 2] = inf | 0x8000
     # row 3: subnormals only
@@ -223,7 +223,7 @@ def test_bf16_huge_values_do_not_overflow(oracle, L, variant):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", range(7, 16))
+@pytest.mark.parametrize("L", range(0, 16))
 def test_deterministic_and_inplace_equals_out_of_place(L, dtype, variant):
     n = 1 << L
     m = 4096 >> max(0, L - 10) if L <= 12 else 9

@@ -2,6 +2,7 @@
 from __future__ import annotations
 
 import numpy as np
+import pytest
 import torch
 
 from paper_2412_08832_amd import workloads as W
@@ -61,3 +62,13 @@ def test_strided_canary_fill():
     bits = W.random_rows(4, 128, "fp16", seed=1, stride=136, fill_bits=0xBEEF)
     assert bits.shape == (4, 136)
     assert (bits[:, 128:] == 0xBEEF).all()
+
+
+def test_small_sweep_points():
+    for k in range(0, 7):
+        w = W.sweep_point(k, "bf16", False)
+        assert (w.m, w.n) == (1 << (28 - k), 1 << k)
+        head = W.generate(w, rows=16)
+        assert head.shape == (16, 1 << k) and np.array_equal(head, W.generate(w, rows=16))
+    with pytest.raises(ValueError):
+        W.sweep_point(16, "fp16", True)
