@@ -930,6 +930,51 @@ __global__ __launch_bounds__(256) void fwht_row_kernel(const uint16_t *in, int64
   }
 }
 
+// n <= 4 with dense rows (both strides equal to n): the rows form one
+// contiguous array of m*n elements, so each thread takes 8 consecutive
+// elements -- 8/n whole rows -- with one 16-byte load and store, like the wider
+// kernels.  A final partial chunk (m*n not a multiple of 8, still whole rows)
+// is read and written element by element.
+template <int DT, int L, bool NT>
+__global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uint16_t *out,
+                                                         int64_t total, ScaleArgs sc) {
+  const int64_t base = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
+  if (base >= total) return;
+  const int count = total - base >= 8 ? 8 : (int)(total - base);  // a multiple of 2^L
+  uint32_t h[8];
+  if (count == 8) {
+    unpack16<8>(gload<NT>(in + base), h);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) h[j] = j < count ? in[base + j] : 0u;
+  }
+  float v[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v[j] = widen1<DT>(h[j]) * sc.scale;
+#pragma unroll
+  for (int b = 0; b < L; ++b) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if ((j & (1 << b)) == 0) {
+        const float a = v[j], c = v[j + (1 << b)];
+        v[j] = a + c;
+        v[j + (1 << b)] = a - c;
+      }
+    }
+  }
+  u4 r;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) r[q] = narrow<DT>(v[2 * q], v[2 * q + 1], 0u);
+  if (count == 8) {
+    gstore<NT>(out + base, r);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (j < count) out[base + j] = (uint16_t)(r[j / 2] >> (16 * (j % 2)));
+    }
+  }
+}
+
 // 16-byte streaming copy, one access per thread, the bandwidth reference for
 // the transform.
 __global__ __launch_bounds__(256) void stream_copy_kernel(const uint16_t *src, uint16_t *dst,
@@ -962,7 +1007,17 @@ ScaleArgs split_scale(float scale, int dtype) {
 template <int DT, int L, int C, int T, int WPB, int HALVES, int FRONT, int EPI = kStore16>
 hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
                       int64_t m, const ScaleArgs &sc, hipStream_t stream, QuantOut qo = {}) {
-  if constexpr (L <= 3) {
+  if constexpr (L <= 2 && EPI == kStore16) {
+    if (in_stride == (1 << L) && out_stride == (1 << L)) {
+      const int64_t total = m << L;
+      hipLaunchKernelGGL((fwht_dense_kernel<DT, L, true>),
+                         dim3((uint32_t)((total + 8 * 256 - 1) / (8 * 256))), dim3(256), 0, stream,
+                         in, out, total, sc);
+    } else {
+      hipLaunchKernelGGL((fwht_row_kernel<DT, L, true, EPI>), dim3((uint32_t)((m + 255) / 256)),
+                         dim3(256), 0, stream, in, in_stride, out, out_stride, m, sc, qo);
+    }
+  } else if constexpr (L <= 3) {
     hipLaunchKernelGGL((fwht_row_kernel<DT, L, true, EPI>), dim3((uint32_t)((m + 255) / 256)),
                        dim3(256), 0, stream, in, in_stride, out, out_stride, m, sc, qo);
   } else if constexpr ((1 << L) <= 512 * C) {
