@@ -154,6 +154,17 @@ def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0
         ]
         alg_bytes = w.m * w.n * 3 + 4 * w.m          # 16-bit read, 1-byte code write, row scales
         outs = codes
+    elif w.n > 1 << 15:
+        # two passes through an fp32 workspace (shared: the calls run in stream order)
+        outs = ins if w.inplace else [torch.empty_like(first) for _ in range(nbuf)]
+        need = H.hadamard_transform_workspace_size(w.m, w.n)
+        ws = torch.empty(need, dtype=torch.uint8, device=d.dev)
+        calls = [
+            (lambda i=i: H.hadamard_transform_ws(ins[i].data_ptr(), w.n, outs[i].data_ptr(), w.n,
+                                                 w.m, w.n, code, w.scale, ws.data_ptr(), need, s))
+            for i in range(nbuf)
+        ]
+        alg_bytes = 2 * nbytes                      # one read + one write of every element
     else:
         outs = ins if w.inplace else [torch.empty_like(first) for _ in range(nbuf)]
         calls = [
@@ -286,8 +297,9 @@ def main(argv=None) -> int:
         for inplace in (True, False):
             for dt in ("fp16", "bf16"):
                 points += [W.sweep_point(k, dt, inplace) for k in range(7, 16)]
-        # sizes below the paper's range: bf16, both modes
+        # sizes below and above the paper's range: bf16 (above: in place, two passes)
         points += [W.sweep_point(k, "bf16", ip) for ip in (True, False) for k in range(0, 7)]
+        points += [W.sweep_point(k, "bf16", True) for k in range(16, 21)]
         q_points = [W.sweep_point(k, "bf16", False) for k in range(0, 16)]
         q_points += [W.WORKLOADS["bf16_1048576x128_inplace"], W.WORKLOADS["fp16_16384x4096"]]
         jobs = [(p, None) for p in points] + [(p, q) for q in ("fp8", "int8") for p in q_points]

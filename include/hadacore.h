@@ -76,6 +76,7 @@ typedef int32_t hadacore_status;
 #define HADACORE_ERROR_LAUNCH 7             /* the HIP runtime rejected the kernel launch */
 #define HADACORE_ERROR_UNSUPPORTED_DEVICE 8 /* current device is not gfx950 */
 #define HADACORE_ERROR_TOO_LARGE 9          /* m too large for one launch (m >= 2^31) */
+#define HADACORE_ERROR_WORKSPACE 10         /* workspace NULL or below the required size */
 
 /*
  * hadamard_transform -- out = scale * in * H_n for m dense rows of n elements.
@@ -103,6 +104,38 @@ hadacore_status hadamard_transform(const void *in, void *out, int64_t m, int64_t
 hadacore_status hadamard_transform_strided(const void *in, int64_t in_row_stride, void *out,
                                            int64_t out_row_stride, int64_t m, int64_t n,
                                            hadacore_dtype dtype, float scale, void *stream);
+
+/*
+ * hadamard_transform_workspace_size -- bytes of device workspace that
+ * hadamard_transform_ws needs for m rows of n elements: 4*m*n (one fp32 value
+ * per element) for 2^15 < n <= 2^20, 0 for n <= 2^15.  Returns 0 as well for
+ * arguments hadamard_transform_ws rejects; the call reports why.
+ */
+int64_t hadamard_transform_workspace_size(int64_t m, int64_t n);
+
+/*
+ * hadamard_transform_ws -- as hadamard_transform_strided, for n up to 2^20.
+ * Sizes above 2^15 lie beyond the paper's range (Sec. 3.2 bounds it at 2^15)
+ * and do not fit one workgroup's registers and LDS, so they run in two passes
+ * through a caller-provided fp32 workspace: pass 1 applies `scale` and the
+ * stages on index bits 15..log2(n)-1 (between the 2^15-element blocks of a
+ * row), pass 2 the stages on bits 0..14 within each block, and rounds once.
+ * Every intermediate stays fp32, so the numerics are those of the one-pass
+ * sizes; the HBM traffic is 12 bytes per element instead of 4.  For n <= 2^15
+ * the call is hadamard_transform_strided and the workspace is not touched.
+ *   workspace        device pointer, 16-byte aligned, at least
+ *                    hadamard_transform_workspace_size(m, n) bytes, not
+ *                    overlapping in or out (NULL allowed for n <= 2^15)
+ *   workspace_bytes  its size in bytes
+ * The workspace is scratch: its contents on return are unspecified, and two
+ * calls in flight at once need two workspaces.  Other arguments, strides,
+ * streams and errors as for hadamard_transform_strided, plus
+ * HADACORE_ERROR_WORKSPACE.  The quantizing entry points stop at n = 2^15.
+ */
+hadacore_status hadamard_transform_ws(const void *in, int64_t in_row_stride, void *out,
+                                      int64_t out_row_stride, int64_t m, int64_t n,
+                                      hadacore_dtype dtype, float scale, void *workspace,
+                                      int64_t workspace_bytes, void *stream);
 
 /*
  * hadamard_transform_fp8 -- the transform fused with per-row quantization to

@@ -725,10 +725,14 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
 // halves the LDS footprint (more workgroups per CU) at the cost of two extra
 // barriers.  The exchange keeps every value in its lane, so the lane layout
 // of the front end carries through to the store.
-template <int DT, int L, int C, int HALVES, bool NT, int FRONT, int EPI>
+//
+// IN32 (second pass of n > 2^15): the input rows are fp32, already scaled, and
+// row r of the input is block r & (2^sub - 1) of output row r >> sub.
+template <int DT, int L, int C, int HALVES, bool NT, int FRONT, int EPI, bool IN32 = false>
 __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
-    const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc,
-    QuantOut qo) {
+    const void *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc,
+    QuantOut qo, int sub) {
+  static_assert(!IN32 || (FRONT == kValu && EPI == kStore16), "fp32 input: VALU, 16-bit output");
   constexpr int n = 1 << L;
   constexpr int NW = n / (512 * C);
   static_assert(NW >= 2 && NW <= C, "wave bits must fit the chunk bits");
@@ -741,16 +745,38 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   const int lane = threadIdx.x & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   const int64_t row = blockIdx.x;
-  const uint16_t *src = in + row * in_stride;
 
-  u4 raw[C];
-  const int lf_load = lane_field_load<FRONT, L>(lane);
-#pragma unroll
-  for (int k = 0; k < C; ++k) {
-    raw[k] = gload_at<NT>(src, (uint32_t)(((w * C + k) * kWave + lf_load) * 16));
-  }
   float v[C * 8];
-  front<DT, FRONT, C>(raw, v, lane, sc.scale, sc.e2);
+  if constexpr (IN32) {
+    // the workspace keeps each 512-element tile G as two 1 KiB halves:
+    // elements G*512 + l*8 + j sit at G*512 + (j/4)*256 + l*4 + j%4 (see
+    // fwht_column_kernel), so both loads of a wave are contiguous
+    const float *src = static_cast<const float *>(in) + row * in_stride;
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      const uint32_t off = (uint32_t)(((w * C + k) * 512 + lane * 4) * 4);
+      // whole-vector bit casts: a bit cast of one ext-vector element reads element 0
+      const f4 lo = __builtin_bit_cast(f4, gload_at<NT>(src, off));
+      const f4 hi = __builtin_bit_cast(f4, gload_at<NT>(src, off + 1024));
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[k * 8 + q] = lo[q];
+        v[k * 8 + 4 + q] = hi[q];
+      }
+    }
+    reg_stage<0>(v);
+    reg_stage<1>(v);
+    reg_stage<2>(v);
+  } else {
+    const uint16_t *src = static_cast<const uint16_t *>(in) + row * in_stride;
+    u4 raw[C];
+    const int lf_load = lane_field_load<FRONT, L>(lane);
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      raw[k] = gload_at<NT>(src, (uint32_t)(((w * C + k) * kWave + lf_load) * 16));
+    }
+    front<DT, FRONT, C>(raw, v, lane, sc.scale, sc.e2);
+  }
   wave_stages<FRONT, L, C>(v, lane);
 
 #pragma unroll
@@ -788,7 +814,7 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   const int lf = lane_field<FRONT, L>(lane);
   if constexpr (EPI == kStore16) {
     const Finisher<DT, FRONT> fin(twisted<FRONT, L>(lane), sc.post);
-    uint16_t *dst = out + row * out_stride;
+    uint16_t *dst = out + (row >> sub) * out_stride + ((row & ((int64_t(1) << sub) - 1)) << L);
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const int W = (k % NW) * C + (k / NW) * NW + w;
@@ -930,6 +956,73 @@ __global__ __launch_bounds__(256) void fwht_row_kernel(const uint16_t *in, int64
   }
 }
 
+// n = A * 2^15 with A = 2..32 (sizes beyond the paper's range), first of two
+// passes: for every row and every group of CW consecutive columns c of the
+// 2^15-element blocks, the A values x[t * 2^15 + c] (t < A) are scaled and
+// run through the stages on index bits 15 and up (butterflies across t), then
+// written as fp32 to the workspace, which holds n floats per row.  The second
+// pass is the n = 2^15 block kernel on those fp32 rows, so every intermediate
+// stays fp32 and the result is rounded once.
+// Workspace layout: within each block, the 512-element tile G (the elements
+// a wave of the second pass loads, 8 per lane) is stored as two 1 KiB halves,
+// element G*512 + l*8 + j at G*512 + (j/4)*256 + l*4 + j%4.  A wave of either
+// pass then covers 1 KiB contiguously per fp32 access.  CW = 8: a thread takes
+// the 8 columns of one lane l of one tile (16-byte load, two 16-byte stores);
+// CW = 4 (A >= 16, to keep A*CW <= 128 values): the 4 columns of one half
+// (8-byte load, one 16-byte store), waves ordered by (tile, half).
+template <int DT, int A, int CW, bool NT>
+__global__ __launch_bounds__(256) void fwht_column_kernel(const uint16_t *in, int64_t in_stride,
+                                                          float *ws, int64_t m, float scale) {
+  static_assert(CW == 8 || CW == 4, "8 or 4 columns per thread");
+  constexpr int kBlock = 1 << 15;
+  constexpr int kGroups = kBlock / CW;
+  typedef typename RowBits<CW>::T T16;
+  const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (g >= m * kGroups) return;
+  const int64_t i = g / kGroups;
+  const int q = (int)(g % kGroups);
+  const int l = q & 63;
+  const int half = CW == 8 ? 0 : (q >> 6) & 1;
+  const int tile = CW == 8 ? q >> 6 : q >> 7;
+  const int c = tile * 512 + l * 8 + half * 4;           // first column
+  const int p = tile * 512 + half * 256 + l * 4;          // its workspace position
+  const uint16_t *src = in + i * in_stride + c;
+  float v[A][CW];
+#pragma unroll
+  for (int t = 0; t < A; ++t) {
+    const T16 *ptr = reinterpret_cast<const T16 *>(src + (int64_t)t * kBlock);
+    const T16 r = NT ? __builtin_nontemporal_load(ptr) : *ptr;
+    uint32_t h[CW];
+    unpack16<CW>(r, h);
+#pragma unroll
+    for (int j = 0; j < CW; ++j) v[t][j] = widen1<DT>(h[j]) * scale;
+  }
+#pragma unroll
+  for (int b = 1; b < A; b <<= 1) {
+#pragma unroll
+    for (int t = 0; t < A; ++t) {
+      if ((t & b) == 0) {
+#pragma unroll
+        for (int j = 0; j < CW; ++j) {
+          const float a = v[t][j], d = v[t + b][j];
+          v[t][j] = a + d;
+          v[t + b][j] = a - d;
+        }
+      }
+    }
+  }
+  float *dst = ws + i * (int64_t)(A * kBlock) + p;
+#pragma unroll
+  for (int t = 0; t < A; ++t) {
+    float *o = dst + (int64_t)t * kBlock;
+#pragma unroll
+    for (int hh = 0; hh < CW / 4; ++hh) {
+      const f4 x = {v[t][4 * hh], v[t][4 * hh + 1], v[t][4 * hh + 2], v[t][4 * hh + 3]};
+      gstore_at<NT>(o, (uint32_t)(hh * 1024), __builtin_bit_cast(u4, x));
+    }
+  }
+}
+
 // n <= 4 with dense rows (both strides equal to n): the rows form one
 // contiguous array of m*n elements, so each thread takes 8 consecutive
 // elements -- 8/n whole rows -- with one 16-byte load and store, like the wider
@@ -1030,7 +1123,7 @@ hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int6
   } else {
     hipLaunchKernelGGL((fwht_block_kernel<DT, L, C, HALVES, true, FRONT, EPI>), dim3((uint32_t)m),
                        dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out, out_stride, sc,
-                       qo);
+                       qo, 0);
   }
   return hipGetLastError();
 }
@@ -1047,7 +1140,7 @@ struct Cfg {
 // MI355X (2^28-element sweeps over chunks per lane, tiles per wave, waves per
 // workgroup, exchange passes and front end, interleaved so that every
 // candidate sees the same clock state).  16-bit output: the smallest per-wave
-// footprint that holds a row wins up to n = 2048, and from n = 4096 a row
+// footprint that holds a row wins up to n = 1024, and from n = 2048 a row
 // spreads over the waves of a workgroup with one LDS exchange.  Quantized
 // output (FP8, INT8) has more arithmetic per byte, so small rows amortize the
 // per-wave setup and the row reduction over two tiles or chunks per wave, and
@@ -1059,7 +1152,8 @@ constexpr Cfg config() {
   } else if constexpr (EPI == kStore16) {
     if constexpr (L <= 9) return {1, 1, 1, 1};
     if constexpr (L == 10) return {2, 1, 1, 1};
-    if constexpr (L == 11 || L == 12) return {4, 1, 1, 1};
+    if constexpr (L == 11) return {2, 1, 1, 1};  // two waves per row, one exchange
+    if constexpr (L == 12) return {4, 1, 1, 1};
     if constexpr (L == 13) return {4, 1, 1, FRONT == kMfma ? 1 : 2};
     if constexpr (L == 14) return {8, 1, 1, FRONT == kMfma ? 1 : 2};
     return {8, 1, 1, 2};
@@ -1079,12 +1173,12 @@ constexpr Cfg config() {
 }
 
 // Front end used unless HADACORE_VARIANT forces one: the matrix cores from
-// n = 2048 for 16-bit output, everywhere from n = 128 for quantized output.
+// n = 4096 for 16-bit output, everywhere from n = 128 for quantized output.
 // Below n = 128 there is only the VALU front (the radix-32 step needs 16 vectors
 // of 32 elements per wave with four lanes per vector row group).
 template <int L, int EPI>
 constexpr int default_front() {
-  return L >= 7 && (EPI != kStore16 || L >= 11) ? kMfma : kValu;
+  return L >= 7 && (EPI != kStore16 || L >= 12) ? kMfma : kValu;
 }
 
 template <int DT, int L, int EPI, int FRONT>
@@ -1135,6 +1229,43 @@ hipError_t launch_dt(int L, const uint16_t *in, int64_t in_stride, uint16_t *out
   }
 }
 
+// n = A * 2^15, A = 2..32: the column pass into the fp32 workspace, then the
+// n = 2^15 block kernel on the workspace rows (fp32 input, VALU front), each
+// writing block t of its output row.
+template <int DT, int A>
+hipError_t launch_large(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
+                        int64_t m, float scale, float *ws, hipStream_t stream) {
+  constexpr int CW = A <= 8 ? 8 : 4;
+  constexpr int kBlock = 1 << 15;
+  const int64_t threads = m * (kBlock / CW);
+  hipLaunchKernelGGL((fwht_column_kernel<DT, A, CW, true>), dim3((uint32_t)((threads + 255) / 256)),
+                     dim3(256), 0, stream, in, in_stride, ws, m, scale);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  constexpr Cfg c = config<15, kStore16, kValu>();
+  constexpr int sub = A == 2 ? 1 : A == 4 ? 2 : A == 8 ? 3 : A == 16 ? 4 : 5;
+  const ScaleArgs unit{1.0f, 1.0f, 0};
+  hipLaunchKernelGGL((fwht_block_kernel<DT, 15, c.C, c.HALVES, true, kValu, kStore16, true>),
+                     dim3((uint32_t)(m * A)), dim3(kBlock / (8 * c.C)), 0, stream,
+                     static_cast<const void *>(ws), (int64_t)kBlock, out, out_stride, unit,
+                     QuantOut{}, sub);
+  return hipGetLastError();
+}
+
+template <int DT>
+hipError_t launch_large_dt(int L, const uint16_t *in, int64_t in_stride, uint16_t *out,
+                           int64_t out_stride, int64_t m, float scale, float *ws,
+                           hipStream_t stream) {
+  switch (L) {
+    case 16: return launch_large<DT, 2>(in, in_stride, out, out_stride, m, scale, ws, stream);
+    case 17: return launch_large<DT, 4>(in, in_stride, out, out_stride, m, scale, ws, stream);
+    case 18: return launch_large<DT, 8>(in, in_stride, out, out_stride, m, scale, ws, stream);
+    case 19: return launch_large<DT, 16>(in, in_stride, out, out_stride, m, scale, ws, stream);
+    case 20: return launch_large<DT, 32>(in, in_stride, out, out_stride, m, scale, ws, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 // HADACORE_VARIANT=valu|mfma forces a front end (testing and tuning); unset,
 // empty or anything else keeps the per-size table.  Read on every call.
 int front_override() {
@@ -1168,6 +1299,9 @@ hadacore_status check_device() {
 // inside a wave tile (at most 32 rows) below 2^32 bytes.
 constexpr int64_t kMaxStride = int64_t(1) << 26;
 
+// Largest log2 n of hadamard_transform_ws (two passes through the workspace).
+constexpr int kMaxLargeL = 20;
+
 int log2_exact(int64_t n) {
   if (n <= 0 || (n & (n - 1)) != 0) return -1;
   int l = 0;
@@ -1184,10 +1318,10 @@ void row_span(const void *p, int64_t stride, int64_t m, int64_t n, uintptr_t *lo
 // Synchronous argument validation shared by the entry points (no HIP calls).
 hadacore_status validate(const void *in, int64_t in_row_stride, const void *out,
                          int64_t out_row_stride, int64_t m, int64_t n, hadacore_dtype dtype,
-                         float scale, int *L_out) {
+                         float scale, int *L_out, int max_L = 15) {
   if (m < 0) return HADACORE_ERROR_INVALID_VALUE;
   const int L = log2_exact(n);
-  if (L < 0 || L > 15) return HADACORE_ERROR_INVALID_SIZE;
+  if (L < 0 || L > max_L) return HADACORE_ERROR_INVALID_SIZE;
   if (dtype != HADACORE_FP16 && dtype != HADACORE_BF16) return HADACORE_ERROR_INVALID_DTYPE;
   if (!isfinite(scale)) return HADACORE_ERROR_INVALID_VALUE;
   const int64_t align = n < 8 ? n : 8;  // rows start on 2*min(n, 8)-byte boundaries
@@ -1235,6 +1369,50 @@ extern "C" hadacore_status hadamard_transform_strided(const void *in, int64_t in
       dtype == HADACORE_FP16
           ? launch_dt<HADACORE_FP16>(L, src, in_row_stride, dst, out_row_stride, m, sc, front, s)
           : launch_dt<HADACORE_BF16>(L, src, in_row_stride, dst, out_row_stride, m, sc, front, s);
+  return err == hipSuccess ? HADACORE_SUCCESS : HADACORE_ERROR_LAUNCH;
+}
+
+extern "C" int64_t hadamard_transform_workspace_size(int64_t m, int64_t n) {
+  const int L = log2_exact(n);
+  if (m <= 0 || L <= 15 || L > kMaxLargeL || m >= (int64_t(1) << 31)) return 0;
+  if (m > (int64_t(1) << 40) / n) return 0;  // the call itself reports TOO_LARGE
+  return 4 * m * n;
+}
+
+extern "C" hadacore_status hadamard_transform_ws(const void *in, int64_t in_row_stride, void *out,
+                                                 int64_t out_row_stride, int64_t m, int64_t n,
+                                                 hadacore_dtype dtype, float scale,
+                                                 void *workspace, int64_t workspace_bytes,
+                                                 void *stream) {
+  int L = 0;
+  const hadacore_status st =
+      validate(in, in_row_stride, out, out_row_stride, m, n, dtype, scale, &L, kMaxLargeL);
+  if (st != HADACORE_SUCCESS || m == 0) return st;
+  if (L <= 15) {
+    return hadamard_transform_strided(in, in_row_stride, out, out_row_stride, m, n, dtype, scale,
+                                      stream);
+  }
+  const int64_t need = hadamard_transform_workspace_size(m, n);
+  if (need == 0) return HADACORE_ERROR_TOO_LARGE;
+  if (workspace == nullptr || workspace_bytes < need) return HADACORE_ERROR_WORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 15) != 0) return HADACORE_ERROR_MISALIGNED;
+  if ((m * (n >> 15)) >= (int64_t(1) << 31)) return HADACORE_ERROR_TOO_LARGE;
+  uintptr_t ilo, ihi, olo, ohi;
+  row_span(in, in_row_stride, m, n, &ilo, &ihi);
+  row_span(out, out_row_stride, m, n, &olo, &ohi);
+  const uintptr_t wlo = reinterpret_cast<uintptr_t>(workspace);
+  const uintptr_t whi = wlo + (uintptr_t)need;
+  if ((wlo < ihi && ilo < whi) || (wlo < ohi && olo < whi)) return HADACORE_ERROR_OVERLAP;
+  const hadacore_status dev = check_device();
+  if (dev != HADACORE_SUCCESS) return dev;
+  const uint16_t *src = static_cast<const uint16_t *>(in);
+  uint16_t *dst = static_cast<uint16_t *>(out);
+  float *ws = static_cast<float *>(workspace);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const hipError_t err =
+      dtype == HADACORE_FP16
+          ? launch_large_dt<HADACORE_FP16>(L, src, in_row_stride, dst, out_row_stride, m, scale, ws, s)
+          : launch_large_dt<HADACORE_BF16>(L, src, in_row_stride, dst, out_row_stride, m, scale, ws, s);
   return err == hipSuccess ? HADACORE_SUCCESS : HADACORE_ERROR_LAUNCH;
 }
 
@@ -1346,6 +1524,8 @@ extern "C" const char *hadacore_status_string(hadacore_status status) {
     case HADACORE_ERROR_LAUNCH: return "kernel launch failed";
     case HADACORE_ERROR_UNSUPPORTED_DEVICE: return "current device is not gfx950";
     case HADACORE_ERROR_TOO_LARGE: return "problem too large for one launch";
+    case HADACORE_ERROR_WORKSPACE:
+      return "workspace missing or smaller than hadamard_transform_workspace_size(m, n)";
     default: return "unknown status";
   }
 }

@@ -24,9 +24,10 @@ SUCCESS = 0
 STATUS_NAMES = {
     0: "SUCCESS", 1: "INVALID_VALUE", 2: "INVALID_SIZE", 3: "INVALID_DTYPE",
     4: "INVALID_STRIDE", 5: "MISALIGNED", 6: "OVERLAP", 7: "LAUNCH",
-    8: "UNSUPPORTED_DEVICE", 9: "TOO_LARGE",
+    8: "UNSUPPORTED_DEVICE", 9: "TOO_LARGE", 10: "WORKSPACE",
 }
-EXPORTS = ("hadamard_transform", "hadamard_transform_strided", "hadamard_transform_fp8",
+EXPORTS = ("hadamard_transform", "hadamard_transform_strided", "hadamard_transform_ws",
+           "hadamard_transform_workspace_size", "hadamard_transform_fp8",
            "hadamard_transform_int8", "hadacore_stream_copy", "hadacore_status_string",
            "hadacore_version")
 
@@ -54,6 +55,10 @@ def library() -> ctypes.CDLL:
         lib.hadamard_transform.restype = i32
         lib.hadamard_transform_strided.argtypes = [vp, i64, vp, i64, i64, i64, i32, f32, vp]
         lib.hadamard_transform_strided.restype = i32
+        lib.hadamard_transform_ws.argtypes = [vp, i64, vp, i64, i64, i64, i32, f32, vp, i64, vp]
+        lib.hadamard_transform_ws.restype = i32
+        lib.hadamard_transform_workspace_size.argtypes = [i64, i64]
+        lib.hadamard_transform_workspace_size.restype = i64
         lib.hadamard_transform_fp8.argtypes = [vp, i64, vp, i64, vp, i64, i64, i32, f32, vp]
         lib.hadamard_transform_fp8.restype = i32
         lib.hadamard_transform_int8.argtypes = [vp, i64, vp, i64, vp, i64, i64, i32, f32, vp]
@@ -89,6 +94,20 @@ def hadamard_transform_strided(in_ptr: int, in_row_stride: int, out_ptr: int,
     if check:
         _check(st, "hadamard_transform_strided")
     return st
+
+
+def hadamard_transform_ws(in_ptr: int, in_row_stride: int, out_ptr: int, out_row_stride: int,
+                          m: int, n: int, dtype: int, scale: float, workspace_ptr: int,
+                          workspace_bytes: int, stream: int = 0, check: bool = True) -> int:
+    st = library().hadamard_transform_ws(in_ptr, in_row_stride, out_ptr, out_row_stride, m, n,
+                                         dtype, scale, workspace_ptr, workspace_bytes, stream)
+    if check:
+        _check(st, "hadamard_transform_ws")
+    return st
+
+
+def hadamard_transform_workspace_size(m: int, n: int) -> int:
+    return int(library().hadamard_transform_workspace_size(m, n))
 
 
 def hadamard_transform_fp8(in_ptr: int, in_row_stride: int, codes_ptr: int, codes_row_stride: int,
@@ -136,12 +155,16 @@ def _dtype_code(t) -> int:
     raise TypeError(f"expected float16 or bfloat16, got {t.dtype}")
 
 
-def transform(x, out=None, scale: float | None = None, n: int | None = None, stream=None):
+def transform(x, out=None, scale: float | None = None, n: int | None = None, stream=None,
+              workspace=None):
     """out = scale * x @ H_n over the first ``n`` columns of each row of a 2-D tensor.
 
     ``x`` and ``out`` are 2-D float16/bfloat16 ROCm tensors with unit column
     stride; ``out=None`` allocates a new tensor, ``out=x`` runs in place.  The
     default scale is fp32(1/sqrt(n)); the default stream is torch's current one.
+    n above 2^15 runs through ``hadamard_transform_ws``; ``workspace`` (a
+    contiguous ROCm tensor of at least hadamard_transform_workspace_size(m, n)
+    bytes) is allocated here when not given.
     """
     import torch
     if x.dim() != 2 or not x.is_cuda:
@@ -166,8 +189,17 @@ def transform(x, out=None, scale: float | None = None, n: int | None = None, str
     in_stride = x.stride(0) if x.shape[0] > 1 else n
     out_stride = out.stride(0) if out.shape[0] > 1 else n
     with torch.cuda.device(x.device):
-        hadamard_transform_strided(x.data_ptr(), in_stride, out.data_ptr(), out_stride,
-                                   x.shape[0], n, code, scale, stream)
+        if n > 1 << 15:
+            need = hadamard_transform_workspace_size(x.shape[0], n)
+            if workspace is None:
+                workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=x.device)
+            wbytes = workspace.numel() * workspace.element_size()
+            hadamard_transform_ws(x.data_ptr(), in_stride, out.data_ptr(), out_stride,
+                                  x.shape[0], n, code, scale, workspace.data_ptr(), wbytes,
+                                  stream)
+        else:
+            hadamard_transform_strided(x.data_ptr(), in_stride, out.data_ptr(), out_stride,
+                                       x.shape[0], n, code, scale, stream)
     return out
 
 

@@ -108,9 +108,9 @@ WORKLOADS = {w.name: w for w in (_fp16_1024x256(), _bf16_1048576x128_inplace(), 
 
 def sweep_point(k: int, dtype: str, inplace: bool, total_log2: int = 28) -> Workload:
     """Sweep point n = 2^k, m = 2^(total_log2 - k), N(0,1).  The paper's sizes are
-    k = 7..15; k = 0..6 extend the sweep below them."""
-    if not 0 <= k <= 15:
-        raise ValueError("sweep covers n = 2^0 .. 2^15")
+    k = 7..15; k = 0..6 and k = 16..20 extend the sweep below and above them."""
+    if not 0 <= k <= 20:
+        raise ValueError("sweep covers n = 2^0 .. 2^20")
     n = 1 << k
     m = 1 << (total_log2 - k)
     mode = "inplace" if inplace else "outofplace"

@@ -189,3 +189,36 @@ def test_quantized_validation(fmt):
     assert _fp8(0, 128, 0, 128, 0, 0, 128, H.BF16, 1.0, 0) == 0             # m == 0
     assert _fp8(A, 128, C8, 128, S8, -1, 128, H.BF16, 1.0, 0) == 1
     assert len(ok_args) == 10
+
+
+W8 = 1 << 36   # fake workspace
+
+
+def _ws(*args):
+    return H.hadamard_transform_ws(*args, check=False)
+
+
+def test_workspace_size():
+    assert H.hadamard_transform_workspace_size(4, 1 << 16) == 4 * 4 * (1 << 16)
+    assert H.hadamard_transform_workspace_size(3, 1 << 20) == 4 * 3 * (1 << 20)
+    assert H.hadamard_transform_workspace_size(4, 1 << 15) == 0     # one pass, no workspace
+    assert H.hadamard_transform_workspace_size(0, 1 << 16) == 0
+    assert H.hadamard_transform_workspace_size(4, 1 << 21) == 0     # unsupported size
+    assert H.hadamard_transform_workspace_size(4, 3 << 15) == 0
+
+
+@cpu_only
+def test_workspace_entry_validation():
+    n = 1 << 16
+    need = H.hadamard_transform_workspace_size(4, n)
+    assert H.hadamard_transform(A, B, 4, n, H.FP16, 1.0, 0, check=False) == 2  # one-pass entry
+    assert _ws(A, n, B, n, 4, 1 << 21, H.FP16, 1.0, W8, need, 0) == 2          # above 2^20
+    assert _ws(A, n, B, n, 4, n, H.FP16, 1.0, 0, need, 0) == 10                # no workspace
+    assert _ws(A, n, B, n, 4, n, H.FP16, 1.0, W8, need - 16, 0) == 10          # too small
+    assert _ws(A, n, B, n, 4, n, H.FP16, 1.0, W8 + 8, need, 0) == 5            # misaligned
+    assert _ws(A, n, B, n, 4, n, H.FP16, 1.0, A + 64, need, 0) == 6            # overlaps in
+    assert _ws(A, n, B, n, 4, n, H.FP16, 1.0, B - need + 2, need, 0) == 5      # misaligned first
+    assert _ws(A, n, B, n, 4, n, H.FP16, 1.0, B - need + 16, need, 0) == 6     # overlaps out
+    assert _ws(A, n + 4, B, n, 4, n, H.FP16, 1.0, W8, need, 0) == 4            # stride % 8
+    assert _ws(0, n, 0, n, 0, n, H.FP16, 1.0, 0, 0, 0) == 0                    # m == 0
+    assert _ws(A, n, B, n, 4, n, H.FP16, math.inf, W8, need, 0) == 1

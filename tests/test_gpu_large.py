@@ -1,0 +1,130 @@
+"""GPU parity of sizes above 2^15 (two passes through the fp32 workspace) against the oracle.
+
+Same criterion as the one-pass sizes (tests/metrics.py): the workspace keeps
+every intermediate in fp32, so the result is rounded once.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from gpu_util import compare_with_oracle, say, to_device, to_host
+from metrics import bits_to_f64
+from paper_2412_08832_amd import hadacore as H
+from paper_2412_08832_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+DTYPES = ["fp16", "bf16"]
+CODE = {"fp16": H.FP16, "bf16": H.BF16}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    H.library()
+    yield
+    torch.cuda.synchronize()
+
+
+def _run_ws(bits, dtype, scale, n, inplace, out_stride=None, out_fill=0xAAAA, canary=0x5C):
+    """Transform through hadamard_transform_ws; returns output bits and the workspace tail."""
+    import torch
+    m, in_stride = bits.shape
+    x = to_device(bits, dtype)
+    if inplace:
+        out, out_stride = x, in_stride
+    else:
+        out_stride = n if out_stride is None else out_stride
+        out = to_device(np.full((m, out_stride), out_fill, np.uint16), dtype)
+    need = H.hadamard_transform_workspace_size(m, n)
+    ws = torch.full((need + 4096,), canary, dtype=torch.uint8, device="cuda")
+    H.hadamard_transform_ws(x.data_ptr(), in_stride, out.data_ptr(), out_stride, m, n, CODE[dtype],
+                            scale, ws.data_ptr(), need, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    return to_host(out), ws[need:].cpu().numpy()
+
+
+@pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", [16, 17, 18, 19, 20])
+def test_large_sizes(oracle, L, dtype, inplace):
+    n = 1 << L
+    m = 5 if L <= 18 else 3
+    say(f"large n={n} m={m} {dtype} inplace={inplace}")
+    bits = W.random_rows(m, n, dtype, seed=4000 + L)
+    s = W.default_scale(n)
+    out, tail = _run_ws(bits, dtype, s, n, inplace)
+    assert (tail == 0x5C).all(), "workspace written past its size"
+    c = compare_with_oracle(oracle, out, bits, dtype, s, n)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_large_strided_rows_keep_gaps(oracle, dtype):
+    n = 1 << 17
+    m = 4
+    bits = W.random_rows(m, n, dtype, seed=17, stride=n + 24, fill_bits=0x7FC1)
+    s = W.default_scale(n)
+    out, _ = _run_ws(bits, dtype, s, n, False, out_stride=n + 40, out_fill=0x5A5A)
+    assert (out[:, n:] == 0x5A5A).all(), "out-of-place write touched the row gap"
+    c = compare_with_oracle(oracle, out[:, :n], bits, dtype, s, n)
+    assert c.ok, str(c)
+    out2, _ = _run_ws(bits, dtype, s, n, True)
+    assert (out2[:, n:] == 0x7FC1).all(), "in-place write touched the row gap"
+    assert np.array_equal(out2[:, :n], out[:, :n])
+
+
+@pytest.mark.parametrize("L", [16, 18, 20])
+def test_large_special_vectors(L):
+    n = 1 << L
+    rows = np.zeros((3, n), np.uint16)
+    rows[0, 0] = 0x3C00                       # delta -> all ones
+    rows[1, :] = 0x3C00                       # ones -> n e_0
+    k = n // 2 + 12345                         # a Walsh row -> n e_k
+    j = np.arange(n, dtype=np.int64)
+    parity = np.zeros(n, dtype=np.int64)
+    v = j & k
+    while v.any():
+        parity ^= v & 1
+        v >>= 1
+    rows[2] = np.where(parity == 1, 0xBC00, 0x3C00).astype(np.uint16)
+    s = 2.0 ** -(L // 2)
+    out, _ = _run_ws(rows, "fp16", s, n, False)
+    y = bits_to_f64(out, "fp16")
+    assert np.array_equal(y[0], np.full(n, s))
+    e0 = np.zeros(n)
+    e0[0] = n * s
+    assert np.array_equal(y[1], e0)
+    ek = np.zeros(n)
+    ek[k] = n * s
+    assert np.array_equal(y[2], ek)
+
+
+def test_large_deterministic_and_wrapper():
+    import torch
+    n = 1 << 18
+    bits = W.random_rows(4, n, "bf16", seed=99)
+    a, _ = _run_ws(bits, "bf16", W.default_scale(n), n, False)
+    b, _ = _run_ws(bits, "bf16", W.default_scale(n), n, True)
+    assert np.array_equal(a, b)
+    x = to_device(bits, "bf16")
+    y = H.transform(x)                         # allocates its own workspace
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(y), a)
+
+
+def test_one_pass_sizes_through_the_workspace_entry(oracle):
+    """n <= 2^15 through hadamard_transform_ws needs no workspace and matches the one-pass call."""
+    import torch
+    n = 1 << 12
+    bits = W.random_rows(33, n, "fp16", seed=5)
+    x = to_device(bits, "fp16")
+    out = torch.empty_like(x)
+    H.hadamard_transform_ws(x.data_ptr(), n, out.data_ptr(), n, 33, n, H.FP16, W.default_scale(n),
+                            0, 0, torch.cuda.current_stream().cuda_stream)
+    ref = H.transform(x)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)

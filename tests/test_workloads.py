@@ -70,5 +70,6 @@ def test_small_sweep_points():
         assert (w.m, w.n) == (1 << (28 - k), 1 << k)
         head = W.generate(w, rows=16)
         assert head.shape == (16, 1 << k) and np.array_equal(head, W.generate(w, rows=16))
+    assert W.sweep_point(20, "fp16", True).m == 256
     with pytest.raises(ValueError):
-        W.sweep_point(16, "fp16", True)
+        W.sweep_point(21, "fp16", True)
