@@ -1148,7 +1148,12 @@ struct Cfg {
 template <int L, int EPI, int FRONT>
 constexpr Cfg config() {
   if constexpr (L <= 6) {
-    return {1, 1, 1, 1};  // n <= 8: one row per thread; n = 16..64: one tile per wave
+    // n <= 8: one row per thread (C, T unused); n = 16..64: one tile per wave for
+    // 16-bit output, while quantized output spreads the per-wave setup and row
+    // reduction over four tiles (n = 16) or two chunks per lane (n = 32, 64)
+    if constexpr (EPI == kStore16 || L <= 3) return {1, 1, 1, 1};
+    if constexpr (L == 4) return {1, 4, 1, 1};
+    return {2, 1, 1, 1};
   } else if constexpr (EPI == kStore16) {
     if constexpr (L <= 9) return {1, 1, 1, 1};
     if constexpr (L == 10) return {2, 1, 1, 1};
