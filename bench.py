@@ -9,7 +9,7 @@ Default workload: bf16, m = 8 x 32 x 4096 = 1,048,576 rows of n = 128 (the
 attention head_dim rotation), in place, scale fp32(1/sqrt(128)).
 
 Prints ONE JSON line.  ``--sweep FILE`` additionally times every named
-workload and the n = 2^7..2^15 sweep (both dtypes, both modes) and writes one
+workload and the n = 2^7..2^16 sweep (both dtypes, both modes) and writes one
 JSON line per point to FILE.
 """
 from __future__ import annotations
@@ -154,7 +154,7 @@ def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0
         ]
         alg_bytes = w.m * w.n * 3 + 4 * w.m          # 16-bit read, 1-byte code write, row scales
         outs = codes
-    elif w.n > 1 << 15:
+    elif w.n > 1 << 16:
         # two passes through an fp32 workspace (shared: the calls run in stream order)
         outs = ins if w.inplace else [torch.empty_like(first) for _ in range(nbuf)]
         need = H.hadamard_transform_workspace_size(w.m, w.n)
@@ -296,11 +296,11 @@ def main(argv=None) -> int:
         points = [W.WORKLOADS[k] for k in ("fp16_1024x256", "bf16_1048576x128_inplace", "fp16_16384x4096", "bf16_4096x32768_inplace")]
         for inplace in (True, False):
             for dt in ("fp16", "bf16"):
-                points += [W.sweep_point(k, dt, inplace) for k in range(7, 16)]
-        # sizes below and above the paper's range: bf16 (above: in place, two passes)
+                points += [W.sweep_point(k, dt, inplace) for k in range(7, 17)]
+        # sizes below and above the one-pass range: bf16 (above: in place, two passes)
         points += [W.sweep_point(k, "bf16", ip) for ip in (True, False) for k in range(0, 7)]
-        points += [W.sweep_point(k, "bf16", True) for k in range(16, 21)]
-        q_points = [W.sweep_point(k, "bf16", False) for k in range(0, 16)]
+        points += [W.sweep_point(k, "bf16", True) for k in range(17, 21)]
+        q_points = [W.sweep_point(k, "bf16", False) for k in range(0, 17)]
         q_points += [W.WORKLOADS["bf16_1048576x128_inplace"], W.WORKLOADS["fp16_16384x4096"]]
         jobs = [(p, None) for p in points] + [(p, q) for q in ("fp8", "int8") for p in q_points]
         with open(args.sweep, "w") as f:

@@ -10,9 +10,10 @@
  * i.e. each row is multiplied on the right by the Sylvester-ordered
  * Walsh-Hadamard matrix H_n (natural order, +-1 entries), and by `scale`.
  * The normalized transform of the paper is scale = 1/sqrt(n); H_n is never
- * stored.  n is a power of two from 1 to 2^15: the paper's sizes are 2^7 to
- * 2^15 (Sec. 2.3-2.4 and Sec. 3.2 bound them at 2^15); the smaller ones are
- * supported as well (n = 1 is the identity times `scale`).  In-place operation
+ * stored.  n is a power of two from 1 to 2^16: the paper's sizes are 2^7 to
+ * 2^15 (Sec. 2.3-2.4 and Sec. 3.2 bound them at 2^15); the smaller ones and
+ * 2^16 are supported as well (n = 1 is the identity times `scale`), and
+ * hadamard_transform_ws goes on to 2^20.  In-place operation
  * (Appendix B) is supported.
  *
  * Numerics: inputs are scaled before any addition -- by `scale`, or by its
@@ -59,7 +60,7 @@
 extern "C" {
 #endif
 
-#define HADACORE_VERSION 10000 /* 1.0.0 */
+#define HADACORE_VERSION 10100 /* 1.1.0: one-pass n = 2^16 */
 
 typedef int32_t hadacore_dtype;
 #define HADACORE_FP16 0 /* IEEE binary16 */
@@ -68,7 +69,7 @@ typedef int32_t hadacore_dtype;
 typedef int32_t hadacore_status;
 #define HADACORE_SUCCESS 0
 #define HADACORE_ERROR_INVALID_VALUE 1      /* m < 0, null pointer with m > 0, non-finite scale */
-#define HADACORE_ERROR_INVALID_SIZE 2       /* n not a power of two in [1, 32768] */
+#define HADACORE_ERROR_INVALID_SIZE 2       /* n not a power of two in [1, 65536] (2^20 for _ws) */
 #define HADACORE_ERROR_INVALID_DTYPE 3      /* dtype not HADACORE_FP16 / HADACORE_BF16 */
 #define HADACORE_ERROR_INVALID_STRIDE 4     /* row stride < n, > 2^26, or not a multiple of min(n, 8) */
 #define HADACORE_ERROR_MISALIGNED 5         /* in or out not 16-byte aligned */
@@ -86,7 +87,7 @@ typedef int32_t hadacore_status;
  *          selects in-place operation, any other overlap is rejected
  *   m      number of rows, >= 0; m == 0 returns HADACORE_SUCCESS and enqueues
  *          nothing (pointers may then be NULL)
- *   n      transform length, a power of two in [1, 32768]
+ *   n      transform length, a power of two in [1, 65536]
  *   dtype  HADACORE_FP16 or HADACORE_BF16 (input and output share it)
  *   scale  finite fp32 multiplier; 1/sqrt(n) gives the orthonormal transform
  *   stream hipStream_t to enqueue on (NULL = default stream)
@@ -108,29 +109,29 @@ hadacore_status hadamard_transform_strided(const void *in, int64_t in_row_stride
 /*
  * hadamard_transform_workspace_size -- bytes of device workspace that
  * hadamard_transform_ws needs for m rows of n elements: 4*m*n (one fp32 value
- * per element) for 2^15 < n <= 2^20, 0 for n <= 2^15.  Returns 0 as well for
+ * per element) for 2^16 < n <= 2^20, 0 for n <= 2^16.  Returns 0 as well for
  * arguments hadamard_transform_ws rejects; the call reports why.
  */
 int64_t hadamard_transform_workspace_size(int64_t m, int64_t n);
 
 /*
  * hadamard_transform_ws -- as hadamard_transform_strided, for n up to 2^20.
- * Sizes above 2^15 lie beyond the paper's range (Sec. 3.2 bounds it at 2^15)
- * and do not fit one workgroup's registers and LDS, so they run in two passes
+ * Sizes above 2^16 (the paper's range ends at 2^15, Sec. 3.2) do not fit one
+ * workgroup's registers in fp32, so they run in two passes
  * through a caller-provided fp32 workspace: pass 1 applies `scale` and the
  * stages on index bits 15..log2(n)-1 (between the 2^15-element blocks of a
  * row), pass 2 the stages on bits 0..14 within each block, and rounds once.
  * Every intermediate stays fp32, so the numerics are those of the one-pass
- * sizes; the HBM traffic is 12 bytes per element instead of 4.  For n <= 2^15
+ * sizes; the HBM traffic is 12 bytes per element instead of 4.  For n <= 2^16
  * the call is hadamard_transform_strided and the workspace is not touched.
  *   workspace        device pointer, 16-byte aligned, at least
  *                    hadamard_transform_workspace_size(m, n) bytes, not
- *                    overlapping in or out (NULL allowed for n <= 2^15)
+ *                    overlapping in or out (NULL allowed for n <= 2^16)
  *   workspace_bytes  its size in bytes
  * The workspace is scratch: its contents on return are unspecified, and two
  * calls in flight at once need two workspaces.  Other arguments, strides,
  * streams and errors as for hadamard_transform_strided, plus
- * HADACORE_ERROR_WORKSPACE.  The quantizing entry points stop at n = 2^15.
+ * HADACORE_ERROR_WORKSPACE.  The quantizing entry points stop at n = 2^16.
  */
 hadacore_status hadamard_transform_ws(const void *in, int64_t in_row_stride, void *out,
                                       int64_t out_row_stride, int64_t m, int64_t n,

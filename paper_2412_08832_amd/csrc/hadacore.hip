@@ -1,9 +1,10 @@
 // hadacore.hip -- batched normalized Walsh-Hadamard transform for gfx950.
 //
 // Computes out[i][j] = scale * sum_k (-1)^popcount(j & k) * in[i][k] for
-// 16-bit rows of length n = 2^L, 0 <= L <= 15 (HadaCore, arXiv 2412.08832:
-// the transform of Sec. 2.1-2.2, sizes of Sec. 3.2 -- 2^7 to 2^15 -- plus the
-// smaller ones, in place per Appendix B, fp16 and bf16 per Appendix C).
+// 16-bit rows of length n = 2^L, 0 <= L <= 16 in one pass (HadaCore, arXiv
+// 2412.08832: the transform of Sec. 2.1-2.2, sizes of Sec. 3.2 -- 2^7 to 2^15
+// -- plus the smaller ones and 2^16, in place per Appendix B, fp16 and bf16
+// per Appendix C), and up to 2^20 in two passes through a workspace.
 // Rows of n <= 8 are one per thread (fwht_row_kernel); the tile structure
 // below applies from n = 16.
 //
@@ -385,10 +386,11 @@ __device__ __forceinline__ void front(const u4 (&raw)[C], float (&v)[C * 8], int
 // (tile bits 9.. below L) and the lane bits that still carry element bits.
 template <int FRONT, int L, int C, int N>
 __device__ __forceinline__ void wave_stages(float (&v)[N], int lane) {
-  static_assert(C == 1 || C == 2 || C == 4 || C == 8, "1, 2, 4 or 8 chunks per lane");
+  static_assert(C == 1 || C == 2 || C == 4 || C == 8 || C == 16, "1 to 16 chunks per lane");
   if constexpr (C >= 2 && L > 9) reg_stage<3>(v);
   if constexpr (C >= 4 && L > 10) reg_stage<4>(v);
   if constexpr (C >= 8 && L > 11) reg_stage<5>(v);
+  if constexpr (C >= 16 && L > 12) reg_stage<6>(v);
   constexpr int mask = lane_stage_mask<FRONT, L>();
   if constexpr (mask & 1) lane_stage<0>(v, lane);
   if constexpr (mask & 2) lane_stage<1>(v, lane);
@@ -724,9 +726,12 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
 // exchange in two passes over the two 4-element halves of each chunk, which
 // halves the LDS footprint (more workgroups per CU) at the cost of two extra
 // barriers.  The exchange keeps every value in its lane, so the lane layout
-// of the front end carries through to the store.
+// of the front end carries through to the store.  At n = 65536 (C = 16,
+// NW = 8) a lane holds 128 fp32 values, so the 512 lanes of the workgroup
+// keep the whole row in registers (256 KiB, half the CU's register file) and
+// each exchange pass takes 128 KiB of LDS: one workgroup per CU.
 //
-// IN32 (second pass of n > 2^15): the input rows are fp32, already scaled, and
+// IN32 (second pass of n > 2^16): the input rows are fp32, already scaled, and
 // row r of the input is block r & (2^sub - 1) of output row r >> sub.
 template <int DT, int L, int C, int HALVES, bool NT, int FRONT, int EPI, bool IN32 = false>
 __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
@@ -956,7 +961,7 @@ __global__ __launch_bounds__(256) void fwht_row_kernel(const uint16_t *in, int64
   }
 }
 
-// n = A * 2^15 with A = 2..32 (sizes beyond the paper's range), first of two
+// n = A * 2^15 with A = 4..32 (sizes beyond the paper's range), first of two
 // passes: for every row and every group of CW consecutive columns c of the
 // 2^15-element blocks, the A values x[t * 2^15 + c] (t < A) are scaled and
 // run through the stages on index bits 15 and up (butterflies across t), then
@@ -1080,7 +1085,7 @@ __global__ __launch_bounds__(256) void stream_copy_kernel(const uint16_t *src, u
 
 // Splits the scale for the kMfma front: 2^e2 goes into the 16-bit H_32 operand
 // (a normal number in that dtype), the rest is applied at the end.  fp16 rows
-// cannot overflow fp32 (|x| <= 65504, n <= 2^15), so their operand is +-1.
+// cannot overflow fp32 (|x| <= 65504, n <= 2^16), so their operand is +-1.
 ScaleArgs split_scale(float scale, int dtype) {
   ScaleArgs a{scale, scale, 0};
   if (dtype == HADACORE_BF16 && scale != 0.0f) {
@@ -1161,19 +1166,22 @@ constexpr Cfg config() {
     if constexpr (L == 12) return {4, 1, 1, 1};
     if constexpr (L == 13) return {4, 1, 1, FRONT == kMfma ? 1 : 2};
     if constexpr (L == 14) return {8, 1, 1, FRONT == kMfma ? 1 : 2};
-    return {8, 1, 1, 2};
+    if constexpr (L == 15) return {8, 1, 1, 2};
+    return {16, 1, 1, 2};  // n = 65536: 128 KiB of fp32 per lane group, exchanged in halves
   } else if constexpr (FRONT == kMfma) {
     if constexpr (L == 7) return {2, 1, 1, 1};
     if constexpr (L == 8 || L == 9) return {1, 4, 1, 1};
     if constexpr (L == 10) return {2, 1, 1, 1};
     if constexpr (L == 11 || L == 12) return {8, 1, 1, 1};
-    return {8, 1, 1, 2};
+    if constexpr (L <= 15) return {8, 1, 1, 2};
+    return {16, 1, 1, 2};
   } else {
     if constexpr (L <= 9) return {2, 1, 1, 1};
     if constexpr (L == 10 || L == 11) return {4, 1, 1, 1};
     if constexpr (L == 12) return {8, 1, 1, 1};
     if constexpr (L == 13) return {4, 1, 1, 2};
-    return {8, 1, 1, 2};
+    if constexpr (L <= 15) return {8, 1, 1, 2};
+    return {16, 1, 1, 2};
   }
 }
 
@@ -1230,11 +1238,12 @@ hipError_t launch_dt(int L, const uint16_t *in, int64_t in_stride, uint16_t *out
     case 13: return launch<DT, 13, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
     case 14: return launch<DT, 14, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
     case 15: return launch<DT, 15, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
+    case 16: return launch<DT, 16, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
     default: return hipErrorInvalidValue;
   }
 }
 
-// n = A * 2^15, A = 2..32: the column pass into the fp32 workspace, then the
+// n = A * 2^15, A = 4..32: the column pass into the fp32 workspace, then the
 // n = 2^15 block kernel on the workspace rows (fp32 input, VALU front), each
 // writing block t of its output row.
 template <int DT, int A>
@@ -1248,7 +1257,7 @@ hipError_t launch_large(const uint16_t *in, int64_t in_stride, uint16_t *out, in
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   constexpr Cfg c = config<15, kStore16, kValu>();
-  constexpr int sub = A == 2 ? 1 : A == 4 ? 2 : A == 8 ? 3 : A == 16 ? 4 : 5;
+  constexpr int sub = A == 4 ? 2 : A == 8 ? 3 : A == 16 ? 4 : 5;
   const ScaleArgs unit{1.0f, 1.0f, 0};
   hipLaunchKernelGGL((fwht_block_kernel<DT, 15, c.C, c.HALVES, true, kValu, kStore16, true>),
                      dim3((uint32_t)(m * A)), dim3(kBlock / (8 * c.C)), 0, stream,
@@ -1262,7 +1271,6 @@ hipError_t launch_large_dt(int L, const uint16_t *in, int64_t in_stride, uint16_
                            int64_t out_stride, int64_t m, float scale, float *ws,
                            hipStream_t stream) {
   switch (L) {
-    case 16: return launch_large<DT, 2>(in, in_stride, out, out_stride, m, scale, ws, stream);
     case 17: return launch_large<DT, 4>(in, in_stride, out, out_stride, m, scale, ws, stream);
     case 18: return launch_large<DT, 8>(in, in_stride, out, out_stride, m, scale, ws, stream);
     case 19: return launch_large<DT, 16>(in, in_stride, out, out_stride, m, scale, ws, stream);
@@ -1304,7 +1312,10 @@ hadacore_status check_device() {
 // inside a wave tile (at most 32 rows) below 2^32 bytes.
 constexpr int64_t kMaxStride = int64_t(1) << 26;
 
-// Largest log2 n of hadamard_transform_ws (two passes through the workspace).
+// Largest log2 n of one pass (a row of n = 65536 fills the registers of a
+// 512-thread workgroup in fp32) and of hadamard_transform_ws (two passes
+// through the workspace above that).
+constexpr int kMaxOnePassL = 16;
 constexpr int kMaxLargeL = 20;
 
 int log2_exact(int64_t n) {
@@ -1323,7 +1334,7 @@ void row_span(const void *p, int64_t stride, int64_t m, int64_t n, uintptr_t *lo
 // Synchronous argument validation shared by the entry points (no HIP calls).
 hadacore_status validate(const void *in, int64_t in_row_stride, const void *out,
                          int64_t out_row_stride, int64_t m, int64_t n, hadacore_dtype dtype,
-                         float scale, int *L_out, int max_L = 15) {
+                         float scale, int *L_out, int max_L = kMaxOnePassL) {
   if (m < 0) return HADACORE_ERROR_INVALID_VALUE;
   const int L = log2_exact(n);
   if (L < 0 || L > max_L) return HADACORE_ERROR_INVALID_SIZE;
@@ -1379,7 +1390,7 @@ extern "C" hadacore_status hadamard_transform_strided(const void *in, int64_t in
 
 extern "C" int64_t hadamard_transform_workspace_size(int64_t m, int64_t n) {
   const int L = log2_exact(n);
-  if (m <= 0 || L <= 15 || L > kMaxLargeL || m >= (int64_t(1) << 31)) return 0;
+  if (m <= 0 || L <= kMaxOnePassL || L > kMaxLargeL || m >= (int64_t(1) << 31)) return 0;
   if (m > (int64_t(1) << 40) / n) return 0;  // the call itself reports TOO_LARGE
   return 4 * m * n;
 }
@@ -1393,7 +1404,7 @@ extern "C" hadacore_status hadamard_transform_ws(const void *in, int64_t in_row_
   const hadacore_status st =
       validate(in, in_row_stride, out, out_row_stride, m, n, dtype, scale, &L, kMaxLargeL);
   if (st != HADACORE_SUCCESS || m == 0) return st;
-  if (L <= 15) {
+  if (L <= kMaxOnePassL) {
     return hadamard_transform_strided(in, in_row_stride, out, out_row_stride, m, n, dtype, scale,
                                       stream);
   }
@@ -1436,7 +1447,7 @@ hadacore_status transform_quantized(const void *in, int64_t in_row_stride, void 
                                     int64_t n, hadacore_dtype dtype, float scale, void *stream) {
   if (m < 0) return HADACORE_ERROR_INVALID_VALUE;
   const int L = log2_exact(n);
-  if (L < 0 || L > 15) return HADACORE_ERROR_INVALID_SIZE;
+  if (L < 0 || L > kMaxOnePassL) return HADACORE_ERROR_INVALID_SIZE;
   if (dtype != HADACORE_FP16 && dtype != HADACORE_BF16) return HADACORE_ERROR_INVALID_DTYPE;
   if (!isfinite(scale)) return HADACORE_ERROR_INVALID_VALUE;
   // input rows start on 2*min(n, 8)-byte boundaries, code rows on min(n, 16)
@@ -1520,7 +1531,7 @@ extern "C" const char *hadacore_status_string(hadacore_status status) {
   switch (status) {
     case HADACORE_SUCCESS: return "success";
     case HADACORE_ERROR_INVALID_VALUE: return "invalid value (m < 0, null pointer or non-finite scale)";
-    case HADACORE_ERROR_INVALID_SIZE: return "invalid size (n must be a power of two in [1, 32768])";
+    case HADACORE_ERROR_INVALID_SIZE: return "invalid size (n must be a power of two in [1, 65536], or up to 2^20 with a workspace)";
     case HADACORE_ERROR_INVALID_DTYPE: return "invalid dtype (expected HADACORE_FP16 or HADACORE_BF16)";
     case HADACORE_ERROR_INVALID_STRIDE:
       return "invalid row stride (>= n, <= 2^26, a multiple of min(n, 8) (codes: min(n, 16)))";

@@ -162,7 +162,7 @@ def transform(x, out=None, scale: float | None = None, n: int | None = None, str
     ``x`` and ``out`` are 2-D float16/bfloat16 ROCm tensors with unit column
     stride; ``out=None`` allocates a new tensor, ``out=x`` runs in place.  The
     default scale is fp32(1/sqrt(n)); the default stream is torch's current one.
-    n above 2^15 runs through ``hadamard_transform_ws``; ``workspace`` (a
+    n above 2^16 runs through ``hadamard_transform_ws``; ``workspace`` (a
     contiguous ROCm tensor of at least hadamard_transform_workspace_size(m, n)
     bytes) is allocated here when not given.
     """
@@ -189,7 +189,7 @@ def transform(x, out=None, scale: float | None = None, n: int | None = None, str
     in_stride = x.stride(0) if x.shape[0] > 1 else n
     out_stride = out.stride(0) if out.shape[0] > 1 else n
     with torch.cuda.device(x.device):
-        if n > 1 << 15:
+        if n > 1 << 16:
             need = hadamard_transform_workspace_size(x.shape[0], n)
             if workspace is None:
                 workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=x.device)

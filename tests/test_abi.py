@@ -71,9 +71,9 @@ def _st(*args):
 
 
 @cpu_only
-@pytest.mark.parametrize("n", [0, 3, 6, 100, 127, 129, 3 * 1024, 65536, -128])
+@pytest.mark.parametrize("n", [0, 3, 6, 100, 127, 129, 3 * 1024, 3 << 15, 1 << 17, -128])
 def test_invalid_size(n):
-    assert _st(A, 65536, B, 65536, 4, n, H.FP16, 1.0, 0) == 2
+    assert _st(A, 1 << 17, B, 1 << 17, 4, n, H.FP16, 1.0, 0) == 2
 
 
 @cpu_only
@@ -170,6 +170,7 @@ def test_quantized_validation(fmt):
 
     ok_args = (A, 128, C8, 128, S8, 4, 128, H.BF16, 1.0, 0)
     assert _fp8(A, 128, C8, 128, S8, 4, 100, H.BF16, 1.0, 0) == 2          # size
+    assert _fp8(A, 1 << 17, C8, 1 << 17, S8, 4, 1 << 17, H.BF16, 1.0, 0) == 2  # above 2^16
     assert _fp8(A, 128, C8, 128, S8, 4, 128, 5, 1.0, 0) == 3                # dtype
     assert _fp8(A, 128, C8, 136, S8, 4, 128, H.BF16, 1.0, 0) == 4           # codes stride % 16
     assert _fp8(A, 8, C8, 12, S8, 4, 8, H.BF16, 1.0, 0) == 4                # n = 8: codes % 8
@@ -199,17 +200,18 @@ def _ws(*args):
 
 
 def test_workspace_size():
-    assert H.hadamard_transform_workspace_size(4, 1 << 16) == 4 * 4 * (1 << 16)
+    assert H.hadamard_transform_workspace_size(4, 1 << 17) == 4 * 4 * (1 << 17)
     assert H.hadamard_transform_workspace_size(3, 1 << 20) == 4 * 3 * (1 << 20)
-    assert H.hadamard_transform_workspace_size(4, 1 << 15) == 0     # one pass, no workspace
-    assert H.hadamard_transform_workspace_size(0, 1 << 16) == 0
+    assert H.hadamard_transform_workspace_size(4, 1 << 16) == 0     # one pass, no workspace
+    assert H.hadamard_transform_workspace_size(4, 1 << 15) == 0
+    assert H.hadamard_transform_workspace_size(0, 1 << 17) == 0
     assert H.hadamard_transform_workspace_size(4, 1 << 21) == 0     # unsupported size
     assert H.hadamard_transform_workspace_size(4, 3 << 15) == 0
 
 
 @cpu_only
 def test_workspace_entry_validation():
-    n = 1 << 16
+    n = 1 << 17
     need = H.hadamard_transform_workspace_size(4, n)
     assert H.hadamard_transform(A, B, 4, n, H.FP16, 1.0, 0, check=False) == 2  # one-pass entry
     assert _ws(A, n, B, n, 4, 1 << 21, H.FP16, 1.0, W8, need, 0) == 2          # above 2^20

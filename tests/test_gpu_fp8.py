@@ -56,7 +56,7 @@ def _run_fp8(bits: np.ndarray, dtype: str, scale: float, n: int, codes_stride: i
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", range(0, 16))
+@pytest.mark.parametrize("L", range(0, 17))
 def test_fp8_every_size_ragged(oracle, L, dtype, variant):
     n = 1 << L
     m = (1 << 20 >> L) + 3 if L <= 12 else 21
@@ -84,7 +84,7 @@ def test_fp8_outlier_workloads(oracle, name):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [3, 5, 7, 12, 15])
+@pytest.mark.parametrize("L", [3, 5, 7, 12, 15, 16])
 def test_fp8_special_rows(oracle, L, dtype, variant):
     n = 1 << L
     bits = W.random_rows(6, n, dtype, seed=9)
@@ -107,7 +107,7 @@ def test_fp8_special_rows(oracle, L, dtype, variant):
     assert c.ok, str(c)
 
 
-@pytest.mark.parametrize("L", [2, 5, 7, 9, 13])
+@pytest.mark.parametrize("L", [2, 5, 7, 9, 13, 16])
 def test_fp8_strided_codes_keep_gaps(oracle, L, variant):
     n = 1 << L
     m = 13
@@ -141,7 +141,7 @@ def test_fp8_large_offsets(oracle, n):
     assert c.ok, str(c)
 
 
-@pytest.mark.parametrize("L", [3, 6, 7, 11, 14])
+@pytest.mark.parametrize("L", [3, 6, 7, 11, 14, 16])
 def test_fp8_deterministic_and_consistent_with_transform(L, variant):
     """Repeated calls agree bit for bit; codes times scales track the 16-bit transform."""
     import torch

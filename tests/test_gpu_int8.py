@@ -57,7 +57,7 @@ def _run_int8(bits: np.ndarray, dtype: str, scale: float, n: int, codes_stride: 
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", range(0, 16))
+@pytest.mark.parametrize("L", range(0, 17))
 def test_int8_every_size_ragged(oracle, L, dtype, variant):
     n = 1 << L
     m = (1 << 20 >> L) + 3 if L <= 12 else 21
@@ -85,7 +85,7 @@ def test_int8_outlier_workloads(oracle, name):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [3, 5, 7, 12, 15])
+@pytest.mark.parametrize("L", [3, 5, 7, 12, 15, 16])
 def test_int8_special_rows(oracle, L, dtype, variant):
     n = 1 << L
     bits = W.random_rows(6, n, dtype, seed=9)
@@ -110,7 +110,7 @@ def test_int8_special_rows(oracle, L, dtype, variant):
     assert c.ok, str(c)
 
 
-@pytest.mark.parametrize("L", [2, 5, 7, 9, 13])
+@pytest.mark.parametrize("L", [2, 5, 7, 9, 13, 16])
 def test_int8_strided_codes_keep_gaps(oracle, L, variant):
     n = 1 << L
     m = 13
@@ -122,7 +122,7 @@ def test_int8_strided_codes_keep_gaps(oracle, L, variant):
     assert c.ok, str(c)
 
 
-@pytest.mark.parametrize("L", [3, 6, 7, 11, 14])
+@pytest.mark.parametrize("L", [3, 6, 7, 11, 14, 16])
 def test_int8_deterministic_and_consistent_with_transform(L, variant):
     """Repeated calls agree bit for bit; codes times scales track the 16-bit transform."""
     import torch

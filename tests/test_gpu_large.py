@@ -1,6 +1,8 @@
-"""GPU parity of sizes above 2^15 (two passes through the fp32 workspace) against the oracle.
+"""GPU parity of hadamard_transform_ws against the oracle: n = 2^17 .. 2^20 run
+in two passes through the fp32 workspace, n = 2^16 (the largest one-pass size)
+is reached through the same entry.
 
-Same criterion as the one-pass sizes (tests/metrics.py): the workspace keeps
+Same criterion as the other sizes (tests/metrics.py): the workspace keeps
 every intermediate in fp32, so the result is rounded once.
 """
 from __future__ import annotations
@@ -116,10 +118,11 @@ def test_large_deterministic_and_wrapper():
     assert np.array_equal(to_host(y), a)
 
 
-def test_one_pass_sizes_through_the_workspace_entry(oracle):
-    """n <= 2^15 through hadamard_transform_ws needs no workspace and matches the one-pass call."""
+@pytest.mark.parametrize("n", [1 << 12, 1 << 16])
+def test_one_pass_sizes_through_the_workspace_entry(n):
+    """n <= 2^16 through hadamard_transform_ws needs no workspace and matches the one-pass call."""
     import torch
-    n = 1 << 12
+    assert H.hadamard_transform_workspace_size(33, n) == 0
     bits = W.random_rows(33, n, "fp16", seed=5)
     x = to_device(bits, "fp16")
     out = torch.empty_like(x)

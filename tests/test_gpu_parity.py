@@ -67,7 +67,7 @@ def _ragged_rows(L: int) -> int:
 
 @pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", range(0, 16))
+@pytest.mark.parametrize("L", range(0, 17))
 def test_every_size_ragged(oracle, L, dtype, inplace, variant):
     n = 1 << L
     m = _ragged_rows(L)
@@ -92,7 +92,7 @@ def test_configs_full_size(oracle, name):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [1, 4, 6] + list(range(7, 16)))
+@pytest.mark.parametrize("L", [1, 4, 6] + list(range(7, 17)))
 def test_sweep_full_size_sampled(oracle, L, dtype):
     w = W.sweep_point(L, dtype, inplace=True)
     say(f"sweep {w.name} (sampled rows)")
@@ -106,7 +106,7 @@ def test_sweep_full_size_sampled(oracle, L, dtype):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [0, 2, 5, 7, 8, 11, 12, 13, 15])
+@pytest.mark.parametrize("L", [0, 2, 5, 7, 8, 11, 12, 13, 15, 16])
 def test_single_row(oracle, L, dtype, variant):
     n = 1 << L
     bits = W.random_rows(1, n, dtype, seed=7 + L)
@@ -125,7 +125,7 @@ def test_zero_rows_leaves_output_untouched():
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [1, 3, 5, 7, 9, 12, 14])
+@pytest.mark.parametrize("L", [1, 3, 5, 7, 9, 12, 14, 16])
 def test_strided_rows_keep_gaps(oracle, L, dtype, variant):
     n = 1 << L
     m = 19
@@ -165,7 +165,7 @@ def test_large_offsets(oracle, n, dtype):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [0, 1, 3, 5, 7, 10, 13, 15])
+@pytest.mark.parametrize("L", [0, 1, 3, 5, 7, 10, 13, 15, 16])
 def test_special_vectors(L, dtype, variant):
     n = 1 << L
     one = W.round_to_bits(np.array([1.0], np.float32), dtype)[0]
@@ -189,7 +189,7 @@ def test_special_vectors(L, dtype, variant):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [1, 2, 5, 7, 12, 15])
+@pytest.mark.parametrize("L", [1, 2, 5, 7, 12, 15, 16])
 def test_nonfinite_and_subnormal_inputs(oracle, L, dtype, variant):
     n = 1 << L
     bits = W.random_rows(6, n, dtype, seed=3)
@@ -209,7 +209,7 @@ def test_nonfinite_and_subnormal_inputs(oracle, L, dtype, variant):
     assert c.ok, str(c)
 
 
-@pytest.mark.parametrize("L", [7, 12, 15])
+@pytest.mark.parametrize("L", [7, 12, 15, 16])
 def test_bf16_huge_values_do_not_overflow(oracle, L, variant):
     n = 1 << L
     rng = np.random.default_rng(L)
@@ -223,7 +223,7 @@ def test_bf16_huge_values_do_not_overflow(oracle, L, variant):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", range(0, 16))
+@pytest.mark.parametrize("L", range(0, 17))
 def test_deterministic_and_inplace_equals_out_of_place(L, dtype, variant):
     n = 1 << L
     m = 4096 >> max(0, L - 10) if L <= 12 else 9
