@@ -203,6 +203,11 @@ __device__ __forceinline__ void lane_stage(float (&v)[N], int lane) {
   } else {
 #pragma unroll
     for (int i = 0; i < N; ++i) {
+      // 128 registers per lane (n = 65536): issue the LDS-path permutes in
+      // groups of 16 so that their results do not pile up in registers
+      if constexpr (N >= 128) {
+        if (i % 16 == 0 && i > 0) __builtin_amdgcn_sched_barrier(0);
+      }
       const int x = __builtin_bit_cast(int, v[i]);
       int p;
       if constexpr (LB == 2) {
@@ -720,6 +725,58 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
   }
 }
 
+// Exchange of the NW wave bits with the low log2(NW) chunk bits through LDS
+// (fp32, in HALVES passes over the 4-element halves of each chunk), then the
+// register stages on the exchanged bits.  LDS word address of tile element
+// ((W*64 + l)*8 + 4h + q) in pass p = h / (2 / HALVES) is
+// ((W*(2/HALVES) + h % (2/HALVES))*64 + l)*4 + q, so each 16-byte access of a
+// wave is 1 KiB contiguous and free of bank conflicts.  After the call, chunk
+// k of wave w holds tile chunk W = (k % NW)*C + (k / NW)*NW + w.  `lead`
+// puts a barrier before the first pass (the LDS is reused from an earlier row).
+template <int C, int NW, int HALVES, int N>
+__device__ __forceinline__ void exchange_wave_bits(float (&v)[N], float4 *lds, int w, int lane,
+                                                   bool lead) {
+  static_assert(NW >= 2 && NW <= C && NW <= 8, "wave bits must fit the chunk bits");
+  static_assert(HALVES == 1 || HALVES == 2, "one or two exchange passes");
+  constexpr int kParts = 2 / HALVES;
+#pragma unroll
+  for (int pass = 0; pass < HALVES; ++pass) {
+    if (pass > 0 || lead) __syncthreads();  // earlier reads of the LDS are done
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      const int W = w * C + k;
+#pragma unroll
+      for (int hh = 0; hh < kParts; ++hh) {
+        const int h = pass * kParts + hh;
+        lds[(W * kParts + hh) * kWave + lane] =
+            make_float4(v[k * 8 + 4 * h], v[k * 8 + 4 * h + 1], v[k * 8 + 4 * h + 2],
+                        v[k * 8 + 4 * h + 3]);
+      }
+    }
+    __syncthreads();
+    // read slot (W*kParts + hh)*64 + lane with W = Wk + w: one per-lane base
+    // (w*kParts*64 + lane, from threadIdx.x) plus immediate offsets, rather
+    // than a register per distinct uniform part
+    const float4 *rd = lds + (int)(threadIdx.x + (kParts - 1) * (threadIdx.x & ~(kWave - 1)));
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      const int Wk = (k % NW) * C + (k / NW) * NW;
+#pragma unroll
+      for (int hh = 0; hh < kParts; ++hh) {
+        const int h = pass * kParts + hh;
+        const float4 f = rd[(Wk * kParts + hh) * kWave];
+        v[k * 8 + 4 * h] = f.x;
+        v[k * 8 + 4 * h + 1] = f.y;
+        v[k * 8 + 4 * h + 2] = f.z;
+        v[k * 8 + 4 * h + 3] = f.w;
+      }
+    }
+  }
+  reg_stage<3>(v);
+  if constexpr (NW >= 4) reg_stage<4>(v);
+  if constexpr (NW >= 8) reg_stage<5>(v);
+}
+
 // n = 512*C*NW with NW >= 2 waves per row: one row per workgroup.  After the
 // in-wave stages the wave bits are exchanged with the low log2(NW) chunk bits
 // through LDS (fp32), then finished as register stages.  HALVES = 2 runs the
@@ -740,12 +797,6 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   static_assert(!IN32 || (FRONT == kValu && EPI == kStore16), "fp32 input: VALU, 16-bit output");
   constexpr int n = 1 << L;
   constexpr int NW = n / (512 * C);
-  static_assert(NW >= 2 && NW <= C, "wave bits must fit the chunk bits");
-  static_assert(HALVES == 1 || HALVES == 2, "one or two exchange passes");
-  // LDS word address of tile element ((W*64 + l)*8 + 4h + q) in pass p = h / (2 / HALVES):
-  // ((W*(2/HALVES) + h % (2/HALVES))*64 + l)*4 + q, so each 16-byte access of a wave is
-  // 1 KiB contiguous and free of bank conflicts.
-  constexpr int kParts = 2 / HALVES;
   __shared__ float4 lds[n / 4 / HALVES];
   const int lane = threadIdx.x & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
@@ -783,39 +834,7 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
     front<DT, FRONT, C>(raw, v, lane, sc.scale, sc.e2);
   }
   wave_stages<FRONT, L, C>(v, lane);
-
-#pragma unroll
-  for (int pass = 0; pass < HALVES; ++pass) {
-    if (pass > 0) __syncthreads();  // the previous pass's reads are done
-#pragma unroll
-    for (int k = 0; k < C; ++k) {
-      const int W = w * C + k;
-#pragma unroll
-      for (int hh = 0; hh < kParts; ++hh) {
-        const int h = pass * kParts + hh;
-        lds[(W * kParts + hh) * kWave + lane] =
-            make_float4(v[k * 8 + 4 * h], v[k * 8 + 4 * h + 1], v[k * 8 + 4 * h + 2],
-                        v[k * 8 + 4 * h + 3]);
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < C; ++k) {
-      const int W = (k % NW) * C + (k / NW) * NW + w;
-#pragma unroll
-      for (int hh = 0; hh < kParts; ++hh) {
-        const int h = pass * kParts + hh;
-        const float4 f = lds[(W * kParts + hh) * kWave + lane];
-        v[k * 8 + 4 * h] = f.x;
-        v[k * 8 + 4 * h + 1] = f.y;
-        v[k * 8 + 4 * h + 2] = f.z;
-        v[k * 8 + 4 * h + 3] = f.w;
-      }
-    }
-  }
-  reg_stage<3>(v);
-  if constexpr (NW >= 4) reg_stage<4>(v);
-  if constexpr (NW >= 8) reg_stage<5>(v);
+  exchange_wave_bits<C, NW, HALVES>(v, lds, w, lane, false);
   const int lf = lane_field<FRONT, L>(lane);
   if constexpr (EPI == kStore16) {
     const Finisher<DT, FRONT> fin(twisted<FRONT, L>(lane), sc.post);
@@ -846,6 +865,77 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
     }
     if (threadIdx.x == 0) qo.scales[row] = qz.scale;
   }
+}
+
+// n = 65536, 16-bit output, matrix-core front: the block kernel's row as a
+// persistent loop.  A row fills half the register file and 128 KiB of LDS, so
+// a CU holds one workgroup and, without a loop, its HBM traffic would pause
+// while the row is transformed.  Here the grid is one workgroup per CU; each
+// takes rows blockIdx.x, + gridDim.x, ... and issues the loads of its next row
+// right after the front end of the current one, so they are in flight during
+// the in-wave stages, the exchange and the store.  The 16 chunks of raw data
+// (64 VGPRs) fit beside the 128 fp32 values because every address is a
+// wave-uniform base plus one per-lane offset.  Same arithmetic as the block
+// kernel, so the results are bit-identical.
+
+// One row of the loop: transform `raw` (row `row`), prefetch row `row` +
+// gridDim.x into `raw` when it exists, store; returns whether it did.
+template <int DT, int L, int C, int HALVES, bool NT>
+__device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16_t *in,
+                                         int64_t in_stride, uint16_t *out, int64_t out_stride,
+                                         const ScaleArgs &sc, int64_t m, float4 *lds, int w,
+                                         int lane) {
+  constexpr int NW = (1 << L) / (512 * C);
+  float v[C * 8];
+  front<DT, kMfma, C>(raw, v, lane, sc.scale, sc.e2);
+  // keep the next row's loads after the front end: both sets of raw
+  // registers live at once would not fit
+  __builtin_amdgcn_sched_barrier(0);
+  const int64_t next = row + gridDim.x;
+  const bool more = next < m;
+  if (more) {
+    const uint16_t *src = in + next * in_stride;
+    const uint32_t ld_off = (uint32_t)(lane_field_load<kMfma, L>(lane) * 16);
+#pragma unroll
+    for (int k = 0; k < C; ++k) raw[k] = gload_at<NT>(src + (w * C + k) * 512, ld_off);
+  }
+  wave_stages<kMfma, L, C>(v, lane);
+  exchange_wave_bits<C, NW, HALVES>(v, lds, w, lane, true);
+  const uint32_t st_off = (uint32_t)(lane_field<kMfma, L>(lane) * 16);
+  const Finisher<DT, kMfma> fin(twisted<kMfma, L>(lane), sc.post);
+  uint16_t *dst = out + row * out_stride;
+#pragma unroll
+  for (int k = 0; k < C; ++k) {
+    const int W = (k % NW) * C + (k / NW) * NW + w;
+    gstore_at<NT>(dst + W * 512, st_off, fin(&v[k * 8]));
+  }
+  return more;
+}
+
+template <int DT, int L, int C, int HALVES, bool NT>
+__global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_loop_kernel(
+    const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc,
+    int64_t m) {
+  __shared__ float4 lds[(1 << L) / 4 / HALVES];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  int64_t row = blockIdx.x;
+  u4 raw[C];
+  const uint16_t *src = in + row * in_stride;
+  const uint32_t ld_off = (uint32_t)(lane_field_load<kMfma, L>(lane) * 16);
+#pragma unroll
+  for (int k = 0; k < C; ++k) raw[k] = gload_at<NT>(src + (w * C + k) * 512, ld_off);
+  // The first row is peeled so that the loop is entered, like it is
+  // re-entered, with the next row's loads older than this row's stores: the
+  // compiler's wait before the front end then covers the loads only, not the
+  // stores that follow them.
+  if (!loop_row<DT, L, C, HALVES, NT>(raw, row, in, in_stride, out, out_stride, sc, m, lds, w,
+                                       lane))
+    return;
+  do {
+    row += gridDim.x;
+  } while (loop_row<DT, L, C, HALVES, NT>(raw, row, in, in_stride, out, out_stride, sc, m, lds, w,
+                                           lane));
 }
 
 // n <= 8: one row per thread.  A row is n consecutive 16-bit values, 2n bytes
@@ -1100,6 +1190,8 @@ ScaleArgs split_scale(float scale, int dtype) {
   return a;
 }
 
+int device_cus();
+
 // C: chunks per lane; T: tiles per wave (wave kernel) ; WPB: waves per workgroup
 // (wave kernel); HALVES: LDS exchange passes (block kernel); FRONT: kValu / kMfma.
 template <int DT, int L, int C, int T, int WPB, int HALVES, int FRONT, int EPI = kStore16>
@@ -1125,6 +1217,13 @@ hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int6
     hipLaunchKernelGGL((fwht_wave_kernel<DT, L, C, T, WPB, true, FRONT, EPI>),
                        dim3((uint32_t)blocks), dim3(kWave * WPB), 0, stream, in, in_stride, out,
                        out_stride, m, sc, qo);
+  } else if constexpr (L == 16 && FRONT == kMfma && EPI == kStore16) {
+    // one resident workgroup per CU, each looping over rows (the quantized
+    // epilogues do not fit beside the prefetched row and keep the block kernel)
+    const int64_t cus = device_cus();
+    const int64_t blocks = m < cus ? m : cus;
+    hipLaunchKernelGGL((fwht_block_loop_kernel<DT, L, C, HALVES, true>), dim3((uint32_t)blocks),
+                       dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out, out_stride, sc, m);
   } else {
     hipLaunchKernelGGL((fwht_block_kernel<DT, L, C, HALVES, true, FRONT, EPI>), dim3((uint32_t)m),
                        dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out, out_stride, sc,
@@ -1292,6 +1391,7 @@ int front_override() {
 // Architecture check, cached per device: 0 unknown, 1 gfx950, 2 other.
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_arch_state[kMaxDevices];
+std::atomic<int> g_cus[kMaxDevices];
 
 hadacore_status check_device() {
   int dev = 0;
@@ -1304,8 +1404,25 @@ hadacore_status check_device() {
   hipDeviceProp_t prop;
   if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return HADACORE_ERROR_UNSUPPORTED_DEVICE;
   const bool ok = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
-  if (dev < kMaxDevices) g_arch_state[dev].store(ok ? 1 : 2, std::memory_order_relaxed);
+  if (dev < kMaxDevices) {
+    g_cus[dev].store(prop.multiProcessorCount, std::memory_order_relaxed);
+    g_arch_state[dev].store(ok ? 1 : 2, std::memory_order_relaxed);
+  }
   return ok ? HADACORE_SUCCESS : HADACORE_ERROR_UNSUPPORTED_DEVICE;
+}
+
+// Compute units of the current device (the grid of the persistent kernel);
+// check_device() has run before any launch and cached it.
+int device_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < kMaxDevices) {
+    const int c = g_cus[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
+  int c = 0;
+  if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && c > 0)
+    return c;
+  return 256;
 }
 
 // Largest row stride (elements, or bytes for FP8 codes): keeps every offset

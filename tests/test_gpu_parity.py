@@ -105,6 +105,23 @@ def test_sweep_full_size_sampled(oracle, L, dtype):
     assert c.ok, str(c)
 
 
+@pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_n65536_several_rows_per_workgroup(oracle, dtype, inplace, variant):
+    """n = 65536 runs one persistent workgroup per CU (matrix-core front): with
+    m = 2 * CUs + 37 rows each workgroup takes two or three rows in turn."""
+    import torch
+    n = 1 << 16
+    m = 2 * torch.cuda.get_device_properties(0).multi_processor_count + 37
+    say(f"n=65536 m={m} {dtype} inplace={inplace} variant={variant}")
+    bits = W.random_rows(m, n, dtype, seed=616)
+    s = W.default_scale(n)
+    out = _run(bits, dtype, s, n, inplace)
+    c = compare_with_oracle(oracle, out, bits, dtype, s, n)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", [0, 2, 5, 7, 8, 11, 12, 13, 15, 16])
 def test_single_row(oracle, L, dtype, variant):
