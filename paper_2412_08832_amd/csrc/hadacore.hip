@@ -1122,10 +1122,14 @@ __global__ __launch_bounds__(256) void fwht_column_kernel(const uint16_t *in, in
 // contiguous array of m*n elements, so each thread takes 8 consecutive
 // elements -- 8/n whole rows -- with one 16-byte load and store, like the wider
 // kernels.  A final partial chunk (m*n not a multiple of 8, still whole rows)
-// is read and written element by element.
-template <int DT, int L, bool NT>
+// is read and written element by element.  Quantized outputs (codes dense as
+// well) store the 8 codes as one 8-byte access and one scale per row; each row
+// has its own amax and both correctly rounded quotients, as in the row kernel.
+template <int DT, int L, bool NT, int EPI>
 __global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uint16_t *out,
-                                                         int64_t total, ScaleArgs sc) {
+                                                         int64_t total, ScaleArgs sc,
+                                                         QuantOut qo) {
+  constexpr int N = 1 << L;
   const int64_t base = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
   if (base >= total) return;
   const int count = total - base >= 8 ? 8 : (int)(total - base);  // a multiple of 2^L
@@ -1150,15 +1154,49 @@ __global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uin
       }
     }
   }
-  u4 r;
+  if constexpr (EPI == kStore16) {
+    u4 r;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) r[q] = narrow<DT>(v[2 * q], v[2 * q + 1], 0u);
-  if (count == 8) {
-    gstore<NT>(out + base, r);
+    for (int q = 0; q < 4; ++q) r[q] = narrow<DT>(v[2 * q], v[2 * q + 1], 0u);
+    if (count == 8) {
+      gstore<NT>(out + base, r);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (j < count) out[base + j] = (uint16_t)(r[j / 2] >> (16 * (j % 2)));
+      }
+    }
   } else {
+#pragma clang fp contract(off)
+    // rows i0 .. i0 + 8/N - 1; products rounded to fp32 before the conversion
+    const int64_t i0 = base >> L;
+    float w[8];
+    uint32_t keep[2] = {0u, 0u};
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      if (j < count) out[base + j] = (uint16_t)(r[j / 2] >> (16 * (j % 2)));
+    for (int r = 0; r < 8 / N; ++r) {
+      float amax = fabsf(v[r * N]);
+#pragma unroll
+      for (int j = 1; j < N; ++j) amax = fmaxf(amax, fabsf(v[r * N + j]));
+      const RowQuant<kValu, EPI> qz(amax);
+#pragma unroll
+      for (int j = 0; j < N; ++j) w[r * N + j] = v[r * N + j] * qz.mul;
+      // byte mask of this row's codes (INT8 clears rows without a usable scale)
+#pragma unroll
+      for (int j = 0; j < N; ++j) {
+        const int b = r * N + j;
+        keep[b / 4] |= (qz.keep & 0xFFu) << (8 * (b % 4));
+      }
+      if (r * N < count) qo.scales[i0 + r] = qz.scale;
+    }
+    const u2 raw = EPI == kFp8 ? to_e4m3x8(w, 1.0f) : to_int8x8(w, 1.0f, 0xFFFFFFFFu);
+    const u2 c = EPI == kFp8 ? raw : u2{raw.x & keep[0], raw.y & keep[1]};
+    if (count == 8) {
+      gstore8_at<NT>(qo.codes + base, 0u, c);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (j < count) qo.codes[base + j] = (uint8_t)((j < 4 ? c.x : c.y) >> (8 * (j % 4)));
+      }
     }
   }
 }
@@ -1197,12 +1235,13 @@ int device_cus();
 template <int DT, int L, int C, int T, int WPB, int HALVES, int FRONT, int EPI = kStore16>
 hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
                       int64_t m, const ScaleArgs &sc, hipStream_t stream, QuantOut qo = {}) {
-  if constexpr (L <= 2 && EPI == kStore16) {
-    if (in_stride == (1 << L) && out_stride == (1 << L)) {
+  if constexpr (L <= 2) {
+    const int64_t out_pitch = EPI == kStore16 ? out_stride : qo.stride;
+    if (in_stride == (1 << L) && out_pitch == (1 << L)) {
       const int64_t total = m << L;
-      hipLaunchKernelGGL((fwht_dense_kernel<DT, L, true>),
+      hipLaunchKernelGGL((fwht_dense_kernel<DT, L, true, EPI>),
                          dim3((uint32_t)((total + 8 * 256 - 1) / (8 * 256))), dim3(256), 0, stream,
-                         in, out, total, sc);
+                         in, out, total, sc, qo);
     } else {
       hipLaunchKernelGGL((fwht_row_kernel<DT, L, true, EPI>), dim3((uint32_t)((m + 255) / 256)),
                          dim3(256), 0, stream, in, in_stride, out, out_stride, m, sc, qo);
