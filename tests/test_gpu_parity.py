@@ -91,13 +91,25 @@ def test_configs_full_size(oracle, name):
     assert c.ok, str(c)
 
 
+@pytest.mark.parametrize("name", ["fp16_1024x256", "bf16_1048576x128_inplace", "fp16_16384x4096", "bf16_4096x32768_inplace"])
+def test_configs_other_mode_bitwise(name):
+    """Each named workload in the other mode (in place <-> out of place) gives the
+    same bits as its stated mode, which test_configs_full_size checks against the oracle."""
+    w = W.WORKLOADS[name]
+    bits = W.generate(w)
+    a = _run(bits, w.dtype, w.scale, w.n, w.inplace)
+    b = _run(bits, w.dtype, w.scale, w.n, not w.inplace)
+    assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("inplace", [True, False], ids=["inplace", "out"])
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", [1, 4, 6] + list(range(7, 17)))
-def test_sweep_full_size_sampled(oracle, L, dtype):
-    w = W.sweep_point(L, dtype, inplace=True)
+def test_sweep_full_size_sampled(oracle, L, dtype, inplace):
+    w = W.sweep_point(L, dtype, inplace=inplace)
     say(f"sweep {w.name} (sampled rows)")
     bits = W.generate(w)
-    out = _run(bits, dtype, w.scale, w.n, True)
+    out = _run(bits, dtype, w.scale, w.n, inplace)
     rng = np.random.default_rng(L)
     rows = np.unique(np.r_[0, w.m - 1, rng.integers(0, w.m, 256)])
     c = compare_with_oracle(oracle, out, bits, dtype, w.scale, w.n, rows=rows)
