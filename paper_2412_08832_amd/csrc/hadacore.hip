@@ -867,24 +867,26 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   }
 }
 
-// n = 65536, 16-bit output, matrix-core front: the block kernel's row as a
-// persistent loop.  A row fills half the register file and 128 KiB of LDS, so
-// a CU holds one workgroup and, without a loop, its HBM traffic would pause
-// while the row is transformed.  Here the grid is one workgroup per CU; each
-// takes rows blockIdx.x, + gridDim.x, ... and issues the loads of its next row
-// right after the front end of the current one, so they are in flight during
-// the in-wave stages, the exchange and the store.  The 16 chunks of raw data
-// (64 VGPRs) fit beside the 128 fp32 values because every address is a
-// wave-uniform base plus one per-lane offset.  Same arithmetic as the block
-// kernel, so the results are bit-identical.
+// n = 65536, matrix-core front: the block kernel's row as a persistent loop.
+// A row fills half the register file and 128 KiB of LDS, so a CU holds one
+// workgroup and, without a loop, its HBM traffic would pause while the row is
+// transformed.  Here the grid is one workgroup per CU; each takes rows
+// blockIdx.x, + gridDim.x, ... and issues the loads of PRE chunks of its next
+// row right after the front end of the current one, so they are in flight
+// during the in-wave stages, the exchange and the epilogue; the other C - PRE
+// chunks follow the epilogue's stores.  16-bit output prefetches the whole row
+// (16 chunks, 64 VGPRs beside the 128 fp32 values); the FP8/INT8 epilogues
+// need a few more registers and prefetch 12.  They fit because every address
+// is a wave-uniform base plus one per-lane offset.  Same arithmetic as the
+// block kernel, so the results are bit-identical.
 
 // One row of the loop: transform `raw` (row `row`), prefetch row `row` +
 // gridDim.x into `raw` when it exists, store; returns whether it did.
-template <int DT, int L, int C, int HALVES, bool NT>
+template <int DT, int L, int C, int HALVES, bool NT, int EPI, int PRE>
 __device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16_t *in,
                                          int64_t in_stride, uint16_t *out, int64_t out_stride,
-                                         const ScaleArgs &sc, int64_t m, float4 *lds, int w,
-                                         int lane) {
+                                         const ScaleArgs &sc, const QuantOut &qo, int64_t m,
+                                         float4 *lds, float *wave_max, int w, int lane) {
   constexpr int NW = (1 << L) / (512 * C);
   float v[C * 8];
   front<DT, kMfma, C>(raw, v, lane, sc.scale, sc.e2);
@@ -897,26 +899,59 @@ __device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16
     const uint16_t *src = in + next * in_stride;
     const uint32_t ld_off = (uint32_t)(lane_field_load<kMfma, L>(lane) * 16);
 #pragma unroll
-    for (int k = 0; k < C; ++k) raw[k] = gload_at<NT>(src + (w * C + k) * 512, ld_off);
+    for (int k = 0; k < PRE; ++k) raw[k] = gload_at<NT>(src + (w * C + k) * 512, ld_off);
   }
   wave_stages<kMfma, L, C>(v, lane);
   exchange_wave_bits<C, NW, HALVES>(v, lds, w, lane, true);
-  const uint32_t st_off = (uint32_t)(lane_field<kMfma, L>(lane) * 16);
-  const Finisher<DT, kMfma> fin(twisted<kMfma, L>(lane), sc.post);
-  uint16_t *dst = out + row * out_stride;
+  const int lf = lane_field<kMfma, L>(lane);
+  if constexpr (EPI == kStore16) {
+    const Finisher<DT, kMfma> fin(twisted<kMfma, L>(lane), sc.post);
+    uint16_t *dst = out + row * out_stride;
 #pragma unroll
-  for (int k = 0; k < C; ++k) {
-    const int W = (k % NW) * C + (k / NW) * NW + w;
-    gstore_at<NT>(dst + W * 512, st_off, fin(&v[k * 8]));
+    for (int k = 0; k < C; ++k) {
+      const int W = (k % NW) * C + (k / NW) * NW + w;
+      gstore_at<NT>(dst + W * 512, (uint32_t)(lf * 16), fin(&v[k * 8]));
+    }
+  } else {
+    // row amax: registers, lanes, then waves through LDS (the exchange's
+    // barriers order this row's writes of wave_max after the last row's reads)
+    float a = abs_max8(&v[0]);
+#pragma unroll
+    for (int k = 1; k < C; ++k) a = max_with(a, __builtin_bit_cast(int, abs_max8(&v[k * 8])));
+    a = lane_max<0x3F>(a, lane);
+    if (lane == 0) wave_max[w] = a;
+    __syncthreads();
+    a = wave_max[0];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) a = fmaxf(a, wave_max[i]);
+    const RowQuant<kMfma, EPI> qz(a, twisted<kMfma, L>(lane), sc.post, lane);
+    uint8_t *codes = qo.codes + row * qo.stride;
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      const int W = (k % NW) * C + (k / NW) * NW + w;
+      gstore8_at<NT>(codes + W * 512, (uint32_t)(lf * 8), qz.codes(&v[k * 8]));
+    }
+    if (threadIdx.x == 0) qo.scales[row] = qz.scale;
+  }
+  if constexpr (PRE < C) {
+    if (more) {
+      __builtin_amdgcn_sched_barrier(0);
+      const uint16_t *src = in + next * in_stride;
+      const uint32_t ld_off = (uint32_t)(lane_field_load<kMfma, L>(lane) * 16);
+#pragma unroll
+      for (int k = PRE; k < C; ++k) raw[k] = gload_at<NT>(src + (w * C + k) * 512, ld_off);
+    }
   }
   return more;
 }
 
-template <int DT, int L, int C, int HALVES, bool NT>
+template <int DT, int L, int C, int HALVES, bool NT, int EPI>
 __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_loop_kernel(
     const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc,
-    int64_t m) {
+    QuantOut qo, int64_t m) {
+  constexpr int PRE = EPI == kStore16 ? C : 12;
   __shared__ float4 lds[(1 << L) / 4 / HALVES];
+  __shared__ float wave_max[(1 << L) / (512 * C)];
   const int lane = threadIdx.x & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   int64_t row = blockIdx.x;
@@ -929,13 +964,13 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_loop_kernel(
   // re-entered, with the next row's loads older than this row's stores: the
   // compiler's wait before the front end then covers the loads only, not the
   // stores that follow them.
-  if (!loop_row<DT, L, C, HALVES, NT>(raw, row, in, in_stride, out, out_stride, sc, m, lds, w,
-                                       lane))
+  if (!loop_row<DT, L, C, HALVES, NT, EPI, PRE>(raw, row, in, in_stride, out, out_stride, sc, qo,
+                                                  m, lds, wave_max, w, lane))
     return;
   do {
     row += gridDim.x;
-  } while (loop_row<DT, L, C, HALVES, NT>(raw, row, in, in_stride, out, out_stride, sc, m, lds, w,
-                                           lane));
+  } while (loop_row<DT, L, C, HALVES, NT, EPI, PRE>(raw, row, in, in_stride, out, out_stride, sc,
+                                                      qo, m, lds, wave_max, w, lane));
 }
 
 // n <= 8: one row per thread.  A row is n consecutive 16-bit values, 2n bytes
@@ -1256,13 +1291,13 @@ hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int6
     hipLaunchKernelGGL((fwht_wave_kernel<DT, L, C, T, WPB, true, FRONT, EPI>),
                        dim3((uint32_t)blocks), dim3(kWave * WPB), 0, stream, in, in_stride, out,
                        out_stride, m, sc, qo);
-  } else if constexpr (L == 16 && FRONT == kMfma && EPI == kStore16) {
-    // one resident workgroup per CU, each looping over rows (the quantized
-    // epilogues do not fit beside the prefetched row and keep the block kernel)
+  } else if constexpr (L == 16 && FRONT == kMfma) {
+    // one resident workgroup per CU, each looping over rows
     const int64_t cus = device_cus();
     const int64_t blocks = m < cus ? m : cus;
-    hipLaunchKernelGGL((fwht_block_loop_kernel<DT, L, C, HALVES, true>), dim3((uint32_t)blocks),
-                       dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out, out_stride, sc, m);
+    hipLaunchKernelGGL((fwht_block_loop_kernel<DT, L, C, HALVES, true, EPI>),
+                       dim3((uint32_t)blocks), dim3((1 << L) / (8 * C)), 0, stream, in, in_stride,
+                       out, out_stride, sc, qo, m);
   } else {
     hipLaunchKernelGGL((fwht_block_kernel<DT, L, C, HALVES, true, FRONT, EPI>), dim3((uint32_t)m),
                        dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out, out_stride, sc,

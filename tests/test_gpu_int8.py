@@ -85,6 +85,22 @@ def test_int8_outlier_workloads(oracle, name):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
+def test_int8_n65536_several_rows_per_workgroup(oracle, dtype, variant):
+    """n = 65536 runs one persistent workgroup per CU (matrix-core front): with
+    m = 2 * CUs + 37 rows each workgroup takes two or three rows in turn."""
+    import torch
+    n = 1 << 16
+    m = 2 * torch.cuda.get_device_properties(0).multi_processor_count + 37
+    say(f"int8 n=65536 m={m} {dtype} variant={variant}")
+    bits = W.random_rows(m, n, dtype, seed=617)
+    s = W.default_scale(n)
+    codes, scales = _run_int8(bits, dtype, s, n)
+    c = compare_int8(oracle, codes, scales, bits, dtype, s, n)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", [0, 1, 2, 3, 5, 7, 12, 15, 16])
 def test_int8_special_rows(oracle, L, dtype, variant):
     n = 1 << L
