@@ -5,7 +5,8 @@
 // 2412.08832: the transform of Sec. 2.1-2.2, sizes of Sec. 3.2 -- 2^7 to 2^15
 // -- plus the smaller ones and 2^16, in place per Appendix B, fp16 and bf16
 // per Appendix C), and up to 2^20 in two passes through a workspace.
-// Rows of n <= 8 are one per thread (fwht_row_kernel); the tile structure
+// Rows of n <= 8 are one per thread (fwht_row_kernel), or, when n <= 4 and the
+// rows are dense, 8/n rows per thread (fwht_dense_kernel); the tile structure
 // below applies from n = 16.
 //
 // Structure of one launch.  The radix-2 stages of the fast transform (Sec.
@@ -1322,7 +1323,8 @@ struct Cfg {
 // spreads over the waves of a workgroup with one LDS exchange.  Quantized
 // output (FP8, INT8) has more arithmetic per byte, so small rows amortize the
 // per-wave setup and the row reduction over two tiles or chunks per wave, and
-// n = 4096 stays in one wave.
+// n = 4096 stays in one wave.  n = 65536 takes 16 chunks per lane in every
+// case, the only shape whose 512 lanes hold the row.
 template <int L, int EPI, int FRONT>
 constexpr Cfg config() {
   if constexpr (L <= 6) {
@@ -1340,7 +1342,7 @@ constexpr Cfg config() {
     if constexpr (L == 13) return {4, 1, 1, FRONT == kMfma ? 1 : 2};
     if constexpr (L == 14) return {8, 1, 1, FRONT == kMfma ? 1 : 2};
     if constexpr (L == 15) return {8, 1, 1, 2};
-    return {16, 1, 1, 2};  // n = 65536: 128 KiB of fp32 per lane group, exchanged in halves
+    return {16, 1, 1, 2};  // n = 65536: the row in registers, exchanged in two 128 KiB halves
   } else if constexpr (FRONT == kMfma) {
     if constexpr (L == 7) return {2, 1, 1, 1};
     if constexpr (L == 8 || L == 9) return {1, 4, 1, 1};

@@ -5,7 +5,8 @@ kernels of ``libhadacore.so``.  The library is loaded from this package
 directory; if it is missing, every call raises (there is no fallback).
 
 The raw entry points take device addresses as integers and keep the C names:
-``hadamard_transform``, ``hadamard_transform_strided``, ``hadamard_transform_fp8``,
+``hadamard_transform``, ``hadamard_transform_strided``, ``hadamard_transform_ws``,
+``hadamard_transform_workspace_size``, ``hadamard_transform_fp8``,
 ``hadamard_transform_int8``, ``hadacore_stream_copy``, ``hadacore_status_string``,
 ``hadacore_version``.  ``transform``, ``transform_fp8`` and ``transform_int8`` are
 convenience wrappers for 2-D torch tensors on a ROCm device.
