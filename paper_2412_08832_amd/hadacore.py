@@ -237,8 +237,8 @@ def transform_fp8(x, codes=None, scales=None, scale: float | None = None, stream
     """Fused transform + per-row e4m3 quantization of a 2-D float16/bfloat16 tensor.
 
     Returns (codes, scales): codes is a (m, n) torch.uint8 tensor of e4m3 bit
-    patterns (view it as torch.float8_e4m3fn to decode) and scales a (m,)
-    float32 tensor, so that x @ H_n * scale ~ codes.float() * scales[:, None].
+    patterns and scales a (m,) float32 tensor, so that
+    x @ H_n * scale ~ codes.view(torch.float8_e4m3fn).float() * scales[:, None].
     """
     import torch
     return _transform_quantized(x, codes, scales, scale, stream, hadamard_transform_fp8,
