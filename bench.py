@@ -185,6 +185,11 @@ def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0
     ]
     csec = d.time_calls(copies, steps, warmup, min_warm_s) / steps
     copy_gbs = 2 * nbytes / csec / 1e9
+    # the runtime's device-to-device copy of the same bytes (torch's copy_ between
+    # contiguous same-dtype tensors on one device is a hipMemcpyAsync)
+    memcpys = [(lambda i=i: dsts[i].copy_(ins[i])) for i in range(nbuf)]
+    msec = d.time_calls(memcpys, steps, warmup, min_warm_s) / steps
+    memcpy_gbs = 2 * nbytes / msec / 1e9
     del ins, outs, dsts, first, calls
     torch.cuda.empty_cache()
     return {
@@ -192,7 +197,8 @@ def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0
         "n": w.n, "inplace": w.inplace and not quant, "output": quant or w.dtype,
         "steps": steps, "rotating_buffers": nbuf, "ms_per_step": per_launch * 1e3,
         "elements_per_s": w.m * w.n / per_launch, "gbs": gbs, "frac_hbm_peak": gbs / HBM_PEAK_GBS,
-        "copy_gbs": copy_gbs, "frac_of_copy": gbs / copy_gbs, "alg_bytes_per_launch": alg_bytes,
+        "copy_gbs": copy_gbs, "frac_of_copy": gbs / copy_gbs, "memcpy_gbs": memcpy_gbs,
+        "alg_bytes_per_launch": alg_bytes,
     }
 
 
@@ -285,6 +291,7 @@ def main(argv=None) -> int:
             "scale": w.scale, "rotating_buffers": r["rotating_buffers"],
             "achieved_gbs": r["gbs"], "frac_hbm_peak": r["frac_hbm_peak"],
             "copy_gbs": r["copy_gbs"], "frac_of_copy": r["frac_of_copy"],
+            "memcpy_gbs": r["memcpy_gbs"],
         },
         "roofline": {
             "bound": "hbm", "achieved": r["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
