@@ -23,7 +23,10 @@
 //   * chunk and in-chunk bits: register butterflies (a, b) -> (a+b, a-b);
 //   * lane bits: the partner lane's value arrives by DPP (xor 1, xor 2 by
 //     quad_perm; xor 8 by row_ror:8, fused into one v_fmac_f32_dpp), by
-//     ds_swizzle (xor 4, xor 16) or by ds_bpermute (xor 32);
+//     ds_swizzle (xor 4, xor 16) or by ds_bpermute (xor 32).  After the
+//     matrix-core front all lane stages are DPP: partner xor 7
+//     (row_half_mirror) replaces xor 4 through a change of basis
+//     (mfma_lane_stages);
 //   * wave bits (n > 512*C): an LDS exchange swaps the wave bits with the low
 //     chunk bits, after which they are register butterflies too.  The store
 //     uses the exchanged layout, so there is no exchange back.
@@ -223,6 +226,46 @@ __device__ __forceinline__ void lane_stage(float (&v)[N], int lane) {
   }
 }
 
+// The four lane stages of the matrix-core front (vector bits on lane bits 0-3)
+// all by DPP.  There is no DPP pattern for partner l ^ 4, but row_half_mirror
+// gives l ^ 7, and the butterflies of a Walsh-Hadamard transform may run along
+// any basis of the index space: with partners l ^ b for b = 1, 2, 7, 8, and
+// lane l "high" in the stage along b_i where <psi_i, l> is odd, psi_i being
+// the dual basis (masks 5, 6, 4, 8), lane p ends up holding
+// (-1)^popcount(p) * y[j(p)] with j(p) = (p0^p2, p1^p2, p0^p1^p2, p3) (bits
+// 0-3).  The sign is the usual twist over lane bits 0-3; j only moves where a
+// lane's result is stored (mfma_frequency).
+template <int PHI>
+__device__ __forceinline__ float dual_sign(int lane) {
+  const uint32_t odd = (uint32_t)__builtin_popcount(lane & PHI) & 1u;
+  return __builtin_bit_cast(float, 0x3F800000u | (odd << 31));
+}
+
+template <int N>
+__device__ __forceinline__ void mfma_lane_stages(float (&v)[N], int lane) {
+  static_assert(N % 8 == 0, "registers come in chunks of 8");
+  {
+    const float sgn = dual_sign<5>(lane);
+#pragma unroll
+    for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("quad_perm:[1,0,3,2]");
+  }
+  {
+    const float sgn = dual_sign<6>(lane);
+#pragma unroll
+    for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("quad_perm:[2,3,0,1]");
+  }
+  {
+    const float sgn = dual_sign<4>(lane);
+#pragma unroll
+    for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("row_half_mirror");
+  }
+  {
+    const float sgn = dual_sign<8>(lane);
+#pragma unroll
+    for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("row_ror:8");
+  }
+}
+
 // ---- front ends: the stages applied to the raw 16-bit data ----------------------
 //
 // kValu: each lane widens its 16-byte chunk (8 consecutive elements) to fp32,
@@ -262,13 +305,29 @@ __device__ __forceinline__ int lane_field_load(int l) {
   }
 }
 
+// Vector index whose transform lane l holds after the lane stages: mfma_vector
+// itself, or for n >= 512 (four vector bits, dual-basis stages) its image under
+// j(p) = (p0^p2, p1^p2, p0^p1^p2, p3).
+template <int L>
+__device__ __forceinline__ int mfma_frequency(int l) {
+  const int p = mfma_vector<L>(l);
+  if constexpr (L >= 9) {
+    const int p2 = (p >> 2) & 1;
+    const int b0 = (p & 1) ^ p2;
+    const int b1 = ((p >> 1) & 1) ^ p2;
+    return b0 | (b1 << 1) | ((b0 ^ b1 ^ p2) << 2) | (p & 8);
+  } else {
+    return p;
+  }
+}
+
 template <int FRONT, int L>
 __device__ __forceinline__ int lane_field(int l) {
   if constexpr (FRONT == kValu) {
     return l;
   } else {
     const int g = l >> 4;
-    return 4 * mfma_vector<L>(l) + (((g & 1) << 1) | (g >> 1));  // hsel = {0, 2, 1, 3}
+    return 4 * mfma_frequency<L>(l) + (((g & 1) << 1) | (g >> 1));  // hsel = {0, 2, 1, 3}
   }
 }
 
@@ -398,12 +457,17 @@ __device__ __forceinline__ void wave_stages(float (&v)[N], int lane) {
   if constexpr (C >= 8 && L > 11) reg_stage<5>(v);
   if constexpr (C >= 16 && L > 12) reg_stage<6>(v);
   constexpr int mask = lane_stage_mask<FRONT, L>();
-  if constexpr (mask & 1) lane_stage<0>(v, lane);
-  if constexpr (mask & 2) lane_stage<1>(v, lane);
-  if constexpr (mask & 4) lane_stage<2>(v, lane);
-  if constexpr (mask & 8) lane_stage<3>(v, lane);
-  if constexpr (mask & 16) lane_stage<4>(v, lane);
-  if constexpr (mask & 32) lane_stage<5>(v, lane);
+  if constexpr (FRONT == kMfma && L >= 9) {
+    static_assert(mask == 0xF, "four vector bits on lane bits 0-3");
+    mfma_lane_stages(v, lane);
+  } else {
+    if constexpr (mask & 1) lane_stage<0>(v, lane);
+    if constexpr (mask & 2) lane_stage<1>(v, lane);
+    if constexpr (mask & 4) lane_stage<2>(v, lane);
+    if constexpr (mask & 8) lane_stage<3>(v, lane);
+    if constexpr (mask & 16) lane_stage<4>(v, lane);
+    if constexpr (mask & 32) lane_stage<5>(v, lane);
+  }
 }
 
 // Undo the twist (and, for kMfma, apply the part of the scale the front end
@@ -877,9 +941,9 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
 // during the in-wave stages, the exchange and the epilogue; the other C - PRE
 // chunks follow the epilogue's stores.  16-bit output prefetches the whole row
 // (16 chunks, 64 VGPRs beside the 128 fp32 values); the FP8/INT8 epilogues
-// need a few more registers and prefetch 12.  They fit because every address
-// is a wave-uniform base plus one per-lane offset.  Same arithmetic as the
-// block kernel, so the results are bit-identical.
+// need more registers and prefetch 4 (more spill).  They fit because every
+// address is a wave-uniform base plus one per-lane offset.  Same arithmetic as
+// the block kernel, so the results are bit-identical.
 
 // One row of the loop: transform `raw` (row `row`), prefetch row `row` +
 // gridDim.x into `raw` when it exists, store; returns whether it did.
@@ -950,7 +1014,7 @@ template <int DT, int L, int C, int HALVES, bool NT, int EPI>
 __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_loop_kernel(
     const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc,
     QuantOut qo, int64_t m) {
-  constexpr int PRE = EPI == kStore16 ? C : 12;
+  constexpr int PRE = EPI == kStore16 ? C : 4;
   __shared__ float4 lds[(1 << L) / 4 / HALVES];
   __shared__ float wave_max[(1 << L) / (512 * C)];
   const int lane = threadIdx.x & (kWave - 1);
