@@ -24,9 +24,9 @@
 //   * lane bits: the partner lane's value arrives by DPP (xor 1, xor 2 by
 //     quad_perm; xor 8 by row_ror:8, fused into one v_fmac_f32_dpp), by
 //     ds_swizzle (xor 4, xor 16) or by ds_bpermute (xor 32).  After the
-//     matrix-core front all lane stages are DPP: partner xor 7
-//     (row_half_mirror) replaces xor 4 through a change of basis
-//     (mfma_lane_stages);
+//     matrix-core front a change of basis replaces xor 4 with xor 7
+//     (row_half_mirror), so all its lane stages are DPP, and moves where each
+//     lane stores (lane_stages, lane_frequency);
 //   * wave bits (n > 512*C): an LDS exchange swaps the wave bits with the low
 //     chunk bits, after which they are register butterflies too.  The store
 //     uses the exchanged layout, so there is no exchange back.
@@ -226,43 +226,64 @@ __device__ __forceinline__ void lane_stage(float (&v)[N], int lane) {
   }
 }
 
-// The four lane stages of the matrix-core front (vector bits on lane bits 0-3)
-// all by DPP.  There is no DPP pattern for partner l ^ 4, but row_half_mirror
-// gives l ^ 7, and the butterflies of a Walsh-Hadamard transform may run along
-// any basis of the index space: with partners l ^ b for b = 1, 2, 7, 8, and
-// lane l "high" in the stage along b_i where <psi_i, l> is odd, psi_i being
-// the dual basis (masks 5, 6, 4, 8), lane p ends up holding
-// (-1)^popcount(p) * y[j(p)] with j(p) = (p0^p2, p1^p2, p0^p1^p2, p3) (bits
-// 0-3).  The sign is the usual twist over lane bits 0-3; j only moves where a
-// lane's result is stored (mfma_frequency).
+// Lane stages over the lane bits in MASK.  With DUAL (the matrix-core front)
+// lane bits 0-2 are all done by DPP.  There is no DPP pattern for
+// partner l ^ 4, but row_half_mirror gives l ^ 7, and the butterflies of a
+// Walsh-Hadamard transform may run along any basis of the index space: with
+// partners l ^ b for b = 1, 2, 7 and lane l "high" in the stage along b_i
+// where <psi_i, l> is odd, psi_i being the dual basis (masks 5, 6, 4), lane p
+// ends up holding (-1)^popcount(p & 7) * y[j(p)] with
+// j(p) = (p0^p2, p1^p2, p0^p1^p2) on bits 0-2 (lane_frequency).  The sign is
+// the usual twist; j only moves where a lane's result is stored.  Higher lane
+// bits keep their own stages (xor 8 by DPP, xor 16 and 32 through the LDS
+// unit).  The VALU front keeps the swizzle for xor 4: there it runs beside
+// the VALU in the LDS unit, and the extra DPP stage measured 1% slower.
 template <int PHI>
 __device__ __forceinline__ float dual_sign(int lane) {
   const uint32_t odd = (uint32_t)__builtin_popcount(lane & PHI) & 1u;
   return __builtin_bit_cast(float, 0x3F800000u | (odd << 31));
 }
 
-template <int N>
-__device__ __forceinline__ void mfma_lane_stages(float (&v)[N], int lane) {
+template <int MASK, bool DUAL, int N>
+__device__ __forceinline__ void lane_stages(float (&v)[N], int lane) {
   static_assert(N % 8 == 0, "registers come in chunks of 8");
-  {
-    const float sgn = dual_sign<5>(lane);
+  if constexpr (DUAL && (MASK & 7) == 7) {
+    {
+      const float sgn = dual_sign<5>(lane);
 #pragma unroll
-    for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("quad_perm:[1,0,3,2]");
+      for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("quad_perm:[1,0,3,2]");
+    }
+    {
+      const float sgn = dual_sign<6>(lane);
+#pragma unroll
+      for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("quad_perm:[2,3,0,1]");
+    }
+    {
+      const float sgn = dual_sign<4>(lane);
+#pragma unroll
+      for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("row_half_mirror");
+    }
+  } else {
+    if constexpr (MASK & 1) lane_stage<0>(v, lane);
+    if constexpr (MASK & 2) lane_stage<1>(v, lane);
+    if constexpr (MASK & 4) lane_stage<2>(v, lane);
   }
-  {
-    const float sgn = dual_sign<6>(lane);
-#pragma unroll
-    for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("quad_perm:[2,3,0,1]");
-  }
-  {
-    const float sgn = dual_sign<4>(lane);
-#pragma unroll
-    for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("row_half_mirror");
-  }
-  {
-    const float sgn = dual_sign<8>(lane);
-#pragma unroll
-    for (int i = 0; i < N; i += 8) HC_FMAC_DPP8("row_ror:8");
+  if constexpr (MASK & 8) lane_stage<3>(v, lane);
+  if constexpr (MASK & 16) lane_stage<4>(v, lane);
+  if constexpr (MASK & 32) lane_stage<5>(v, lane);
+}
+
+// Lane position p (bits 0-5) -> the index of the transform output it holds
+// after lane_stages<MASK, DUAL>.
+template <int MASK, bool DUAL>
+__device__ __forceinline__ int lane_frequency(int p) {
+  if constexpr (DUAL && (MASK & 7) == 7) {
+    const int p2 = (p >> 2) & 1;
+    const int b0 = (p & 1) ^ p2;
+    const int b1 = ((p >> 1) & 1) ^ p2;
+    return b0 | (b1 << 1) | ((b0 ^ b1 ^ p2) << 2) | (p & ~7);
+  } else {
+    return p;
   }
 }
 
@@ -305,32 +326,6 @@ __device__ __forceinline__ int lane_field_load(int l) {
   }
 }
 
-// Vector index whose transform lane l holds after the lane stages: mfma_vector
-// itself, or for n >= 512 (four vector bits, dual-basis stages) its image under
-// j(p) = (p0^p2, p1^p2, p0^p1^p2, p3).
-template <int L>
-__device__ __forceinline__ int mfma_frequency(int l) {
-  const int p = mfma_vector<L>(l);
-  if constexpr (L >= 9) {
-    const int p2 = (p >> 2) & 1;
-    const int b0 = (p & 1) ^ p2;
-    const int b1 = ((p >> 1) & 1) ^ p2;
-    return b0 | (b1 << 1) | ((b0 ^ b1 ^ p2) << 2) | (p & 8);
-  } else {
-    return p;
-  }
-}
-
-template <int FRONT, int L>
-__device__ __forceinline__ int lane_field(int l) {
-  if constexpr (FRONT == kValu) {
-    return l;
-  } else {
-    const int g = l >> 4;
-    return 4 * mfma_frequency<L>(l) + (((g & 1) << 1) | (g >> 1));  // hsel = {0, 2, 1, 3}
-  }
-}
-
 // Lane bits that carry element bits still to be processed after the front end
 // (a mask over lane bits 0-5).
 template <int FRONT, int L>
@@ -339,6 +334,20 @@ constexpr int lane_stage_mask() {
     return (1 << (L - 3 >= 6 ? 6 : L - 3)) - 1;
   } else {
     return L == 7 ? 0x3 : (L == 8 ? 0xB : 0xF);
+  }
+}
+
+// Tile bits 3-8 whose transform outputs lane l holds after all lane stages
+// (the store layout; lane_frequency moves bits 0-2 after the basis change).
+template <int FRONT, int L>
+__device__ __forceinline__ int lane_field(int l) {
+  constexpr int mask = lane_stage_mask<FRONT, L>();
+  if constexpr (FRONT == kValu) {
+    return lane_frequency<mask, false>(l);
+  } else {
+    const int g = l >> 4;
+    return 4 * lane_frequency<mask, true>(mfma_vector<L>(l)) +
+           (((g & 1) << 1) | (g >> 1));  // hsel = {0, 2, 1, 3}
   }
 }
 
@@ -456,18 +465,7 @@ __device__ __forceinline__ void wave_stages(float (&v)[N], int lane) {
   if constexpr (C >= 4 && L > 10) reg_stage<4>(v);
   if constexpr (C >= 8 && L > 11) reg_stage<5>(v);
   if constexpr (C >= 16 && L > 12) reg_stage<6>(v);
-  constexpr int mask = lane_stage_mask<FRONT, L>();
-  if constexpr (FRONT == kMfma && L >= 9) {
-    static_assert(mask == 0xF, "four vector bits on lane bits 0-3");
-    mfma_lane_stages(v, lane);
-  } else {
-    if constexpr (mask & 1) lane_stage<0>(v, lane);
-    if constexpr (mask & 2) lane_stage<1>(v, lane);
-    if constexpr (mask & 4) lane_stage<2>(v, lane);
-    if constexpr (mask & 8) lane_stage<3>(v, lane);
-    if constexpr (mask & 16) lane_stage<4>(v, lane);
-    if constexpr (mask & 32) lane_stage<5>(v, lane);
-  }
+  lane_stages<lane_stage_mask<FRONT, L>(), FRONT == kMfma>(v, lane);
 }
 
 // Undo the twist (and, for kMfma, apply the part of the scale the front end
