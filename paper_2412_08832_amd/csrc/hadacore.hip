@@ -339,14 +339,15 @@ constexpr int lane_stage_mask() {
 
 // Tile bits 3-8 whose transform outputs lane l holds after all lane stages
 // (the store layout; lane_frequency moves bits 0-2 after the basis change).
-template <int FRONT, int L>
+// DUAL must match the wave_stages call of the same kernel.
+template <int FRONT, int L, bool DUAL = FRONT == kMfma>
 __device__ __forceinline__ int lane_field(int l) {
   constexpr int mask = lane_stage_mask<FRONT, L>();
   if constexpr (FRONT == kValu) {
-    return lane_frequency<mask, false>(l);
+    return lane_frequency<mask, DUAL>(l);
   } else {
     const int g = l >> 4;
-    return 4 * lane_frequency<mask, true>(mfma_vector<L>(l)) +
+    return 4 * lane_frequency<mask, DUAL>(mfma_vector<L>(l)) +
            (((g & 1) << 1) | (g >> 1));  // hsel = {0, 2, 1, 3}
   }
 }
@@ -458,14 +459,16 @@ __device__ __forceinline__ void front(const u4 (&raw)[C], float (&v)[C * 8], int
 
 // The remaining stages inside one wave: the chunk bits that are element bits
 // (tile bits 9.. below L) and the lane bits that still carry element bits.
-template <int FRONT, int L, int C, int N>
+// DUAL selects the all-DPP lane stages (lane_stages); by default the
+// matrix-core front uses them and the VALU front does not.
+template <int FRONT, int L, int C, bool DUAL = FRONT == kMfma, int N>
 __device__ __forceinline__ void wave_stages(float (&v)[N], int lane) {
   static_assert(C == 1 || C == 2 || C == 4 || C == 8 || C == 16, "1 to 16 chunks per lane");
   if constexpr (C >= 2 && L > 9) reg_stage<3>(v);
   if constexpr (C >= 4 && L > 10) reg_stage<4>(v);
   if constexpr (C >= 8 && L > 11) reg_stage<5>(v);
   if constexpr (C >= 16 && L > 12) reg_stage<6>(v);
-  lane_stages<lane_stage_mask<FRONT, L>(), FRONT == kMfma>(v, lane);
+  lane_stages<lane_stage_mask<FRONT, L>(), DUAL>(v, lane);
 }
 
 // Undo the twist (and, for kMfma, apply the part of the scale the front end
@@ -939,9 +942,9 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
 // during the in-wave stages, the exchange and the epilogue; the other C - PRE
 // chunks follow the epilogue's stores.  16-bit output prefetches the whole row
 // (16 chunks, 64 VGPRs beside the 128 fp32 values); the FP8/INT8 epilogues
-// need more registers and prefetch 4 (more spill).  They fit because every
-// address is a wave-uniform base plus one per-lane offset.  Same arithmetic as
-// the block kernel, so the results are bit-identical.
+// need more registers and prefetch 12.  They fit because every address is a
+// wave-uniform base plus one per-lane offset.  Same arithmetic as the block
+// kernel, so the results are bit-identical.
 
 // One row of the loop: transform `raw` (row `row`), prefetch row `row` +
 // gridDim.x into `raw` when it exists, store; returns whether it did.
@@ -951,6 +954,9 @@ __device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16
                                          const ScaleArgs &sc, const QuantOut &qo, int64_t m,
                                          float4 *lds, float *wave_max, int w, int lane) {
   constexpr int NW = (1 << L) / (512 * C);
+  // the FP8/INT8 epilogues keep the swizzle lane stage: with the all-DPP
+  // stages the compiler's schedule spills unless the prefetch drops to 4 chunks
+  constexpr bool kDual = EPI == kStore16;
   float v[C * 8];
   front<DT, kMfma, C>(raw, v, lane, sc.scale, sc.e2);
   // keep the next row's loads after the front end: both sets of raw
@@ -964,9 +970,9 @@ __device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16
 #pragma unroll
     for (int k = 0; k < PRE; ++k) raw[k] = gload_at<NT>(src + (w * C + k) * 512, ld_off);
   }
-  wave_stages<kMfma, L, C>(v, lane);
+  wave_stages<kMfma, L, C, kDual>(v, lane);
   exchange_wave_bits<C, NW, HALVES>(v, lds, w, lane, true);
-  const int lf = lane_field<kMfma, L>(lane);
+  const int lf = lane_field<kMfma, L, kDual>(lane);
   if constexpr (EPI == kStore16) {
     const Finisher<DT, kMfma> fin(twisted<kMfma, L>(lane), sc.post);
     uint16_t *dst = out + row * out_stride;
@@ -1012,7 +1018,7 @@ template <int DT, int L, int C, int HALVES, bool NT, int EPI>
 __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_loop_kernel(
     const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc,
     QuantOut qo, int64_t m) {
-  constexpr int PRE = EPI == kStore16 ? C : 4;
+  constexpr int PRE = EPI == kStore16 ? C : 12;
   __shared__ float4 lds[(1 << L) / 4 / HALVES];
   __shared__ float wave_max[(1 << L) / (512 * C)];
   const int lane = threadIdx.x & (kWave - 1);
