@@ -36,7 +36,11 @@
  * Streams: work is enqueued asynchronously on `stream` (a hipStream_t; NULL
  * means the default stream) and the call returns without synchronizing.
  * Buffers must stay alive until that work completes.  Faults in the enqueued
- * kernel surface at the caller's next synchronization, not here.
+ * kernel surface at the caller's next synchronization, not here.  A call
+ * enqueues kernel launches only (no allocation, memset or synchronization),
+ * so it can be captured into a HIP graph once the first call on a device has
+ * run outside capture (that call caches the device check); calls on
+ * different streams may run concurrently.
  *
  * Kernels: per transform size the library picks one of two front ends for the
  * first stages, both giving results within fp32 rounding of each other: fp32
