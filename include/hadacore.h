@@ -53,7 +53,8 @@
  * Errors: arguments are validated synchronously before anything is enqueued;
  * on error nothing is enqueued and a nonzero status is returned.  No call
  * aborts or throws.  The library keeps no state beyond a per-device cache of
- * the architecture check and is safe to call from several host threads.
+ * the architecture check and the compute-unit count, and is safe to call from
+ * several host threads.
  */
 #ifndef HADACORE_H
 #define HADACORE_H
