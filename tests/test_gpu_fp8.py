@@ -135,7 +135,7 @@ def test_fp8_strided_codes_keep_gaps(oracle, L, variant):
     assert c.ok, str(c)
 
 
-@pytest.mark.parametrize("n", [256, 4096])
+@pytest.mark.parametrize("n", [256, 4096, 65536])
 def test_fp8_large_offsets(oracle, n):
     """Input rows 2^26 elements and code rows 2^26 bytes apart (the largest strides)."""
     import torch

@@ -172,7 +172,7 @@ def test_strided_rows_keep_gaps(oracle, L, dtype, variant):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("n", [256, 4096])
+@pytest.mark.parametrize("n", [256, 4096, 65536])
 def test_large_offsets(oracle, n, dtype):
     """Rows 2^26 elements apart (the largest stride): row offsets past 2^32 bytes."""
     import torch
