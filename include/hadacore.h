@@ -34,7 +34,9 @@
  * boundary of its access width.
  *
  * Streams: work is enqueued asynchronously on `stream` (a hipStream_t; NULL
- * means the default stream) and the call returns without synchronizing.
+ * means the default stream), which must belong to the current device (the
+ * architecture check and launch shape use it), and the call returns without
+ * synchronizing.
  * Buffers must stay alive until that work completes.  Faults in the enqueued
  * kernel surface at the caller's next synchronization, not here.  A call
  * enqueues kernel launches only (no allocation, memset or synchronization),
