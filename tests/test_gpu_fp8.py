@@ -84,6 +84,20 @@ def test_fp8_outlier_workloads(oracle, name):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", [2, 7, 12, 16])
+def test_fp8_unusual_scales(oracle, L, dtype, variant):
+    """Zero, negative and non-power-of-two scales: a negative scale flips every
+    code, the row scale stays amax / Q >= 0, and a zero scale gives zero rows."""
+    n = 1 << L
+    bits = W.random_rows(11, n, dtype, seed=950 + L)
+    for s in (0.0, -1.0, 3.0, -0.0078125):
+        codes, scales = _run_fp8(bits, dtype, s, n)
+        c = compare_fp8(oracle, codes, scales, bits, dtype, s, n)
+        assert c.ok, f"scale {s}: {c}"
+        assert (scales >= 0).all()
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
 def test_fp8_n65536_several_rows_per_workgroup(oracle, dtype, variant):
     """n = 65536 runs one persistent workgroup per CU (matrix-core front): with
     m = 2 * CUs + 37 rows each workgroup takes two or three rows in turn."""

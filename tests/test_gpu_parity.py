@@ -134,6 +134,25 @@ def test_n65536_several_rows_per_workgroup(oracle, dtype, inplace, variant):
     assert c.ok, str(c)
 
 
+# scales beyond 1/sqrt(n): zero, negative, not a power of two, far from 1 (kept
+# where the outputs stay inside the dtype's range, so that the comparison with
+# the unrounded oracle is meaningful)
+SCALES = {"fp16": [0.0, -1.0, -0.0078125, 3.0, 1e-3], "bf16": [0.0, -1.0, -0.0078125, 3.0, 1e-30, 1e30]}
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("L", [2, 5, 7, 12, 15, 16])
+def test_unusual_scales(oracle, L, dtype, variant):
+    n = 1 << L
+    m = 19
+    bits = W.random_rows(m, n, dtype, seed=900 + L)
+    for s in SCALES[dtype]:
+        s32 = float(np.float32(s))
+        out = _run(bits, dtype, s32, n, False)
+        c = compare_with_oracle(oracle, out, bits, dtype, s32, n)
+        assert c.ok, f"scale {s32}: {c}"
+
+
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", [0, 2, 5, 7, 8, 11, 12, 13, 15, 16])
 def test_single_row(oracle, L, dtype, variant):
