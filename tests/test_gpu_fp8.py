@@ -83,6 +83,28 @@ def test_fp8_outlier_workloads(oracle, name):
     assert c.ok, str(c)
 
 
+@pytest.mark.parametrize("dense", [True, False], ids=["dense", "strided"])
+def test_fp8_n1_scales_bit_exact(oracle, dense):
+    """n = 1: both sides round y = x * scale once to fp32, so the row scale
+    amax / 448 and the codes must match the oracle bit for bit.  The row
+    kernels form amax / 448 by a multiply-and-correct sequence where that is
+    exact and divide elsewhere; the rows span bf16's range, subnormals and the
+    threshold 448 * 2^-126 of the fast path included."""
+    rng = np.random.default_rng(31)
+    m = 4099
+    vals = (rng.choice([-1.0, 1.0], m) * 2.0 ** rng.uniform(-133, 127, m)).astype(np.float32)
+    t = np.float32(448 * 2.0 ** -126)
+    vals[:6] = [0.0, t, np.nextafter(t, np.float32(0)), np.nextafter(t, np.float32(1)), -t, 2.0 ** -130]
+    bits = W.round_to_bits(vals, "bf16")[:, None]
+    if not dense:
+        bits = np.hstack([bits, np.full_like(bits, 0x7FC1)])   # input stride 2: the row kernel
+    for s in (1.0, 0.3700000047683716):
+        codes, scales = _run_fp8(bits, "bf16", s, 1, codes_stride=1 if dense else 2)
+        ref_codes, ref_scales = oracle.fwht_fp8(bits, "bf16", s, n=1)
+        assert np.array_equal(scales.view(np.uint32), ref_scales.view(np.uint32)), f"scale {s}"
+        assert np.array_equal(codes[:, :1].view(np.uint8), ref_codes.view(np.uint8)), f"scale {s}"
+
+
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", [2, 7, 12, 16])
 def test_fp8_unusual_scales(oracle, L, dtype, variant):
