@@ -956,12 +956,13 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
 // transformed.  Here the grid is one workgroup per CU; each takes rows
 // blockIdx.x, + gridDim.x, ... and issues the loads of PRE chunks of its next
 // row right after the front end of the current one, so they are in flight
-// during the in-wave stages, the exchange and the epilogue; the other C - PRE
-// chunks follow the epilogue's stores.  16-bit output prefetches the whole row
-// (16 chunks, 64 VGPRs beside the 128 fp32 values); the FP8/INT8 epilogues
-// need more registers and prefetch 12.  They fit because every address is a
-// wave-uniform base plus one per-lane offset.  Same arithmetic as the block
-// kernel, so the results are bit-identical.
+// during the in-wave stages, the exchange and the epilogue.  16-bit output
+// prefetches the whole row (16 chunks, 64 VGPRs beside the 128 fp32 values);
+// the FP8/INT8 epilogues need more registers and prefetch 14, and issue the
+// last C - PRE chunks between their first code stores, as those free
+// registers.  They fit because every address is a wave-uniform base plus one
+// per-lane offset.  Same arithmetic as the block kernel, so the results are
+// bit-identical.
 
 // One row of the loop: transform `raw` (row `row`), prefetch row `row` +
 // gridDim.x into `raw` when it exists, store; returns whether it did.
@@ -971,9 +972,6 @@ __device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16
                                          const ScaleArgs &sc, const QuantOut &qo, int64_t m,
                                          float4 *lds, float *wave_max, int w, int lane) {
   constexpr int NW = (1 << L) / (512 * C);
-  // the FP8/INT8 epilogues keep the swizzle lane stage: with the all-DPP
-  // stages the compiler's schedule spills unless the prefetch drops to 4 chunks
-  constexpr bool kDual = EPI == kStore16;
   float v[C * 8];
   front<DT, kMfma, C>(raw, v, lane, sc.scale, sc.e2);
   // keep the next row's loads after the front end: both sets of raw
@@ -981,15 +979,24 @@ __device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16
   __builtin_amdgcn_sched_barrier(0);
   const int64_t next = row + gridDim.x;
   const bool more = next < m;
-  if (more) {
+  // The quantized epilogues load without a branch (with the loads under
+  // `if (more)` the register allocator spills beside the row): a workgroup
+  // past its last row reads row m - 1, the same row for every such
+  // workgroup, so those reads come from cache.
+  if (EPI == kStore16 && more) {
     const uint16_t *src = in + next * in_stride;
     const uint32_t ld_off = (uint32_t)(lane_field_load<kMfma, L>(lane) * 16);
 #pragma unroll
     for (int k = 0; k < PRE; ++k) raw[k] = gload_at<NT>(src + (w * C + k) * 512, ld_off);
+  } else if (EPI != kStore16) {
+    const uint16_t *src = in + (more ? next : m - 1) * in_stride;
+    const uint32_t ld_off = (uint32_t)(lane_field_load<kMfma, L>(lane) * 16);
+#pragma unroll
+    for (int k = 0; k < PRE; ++k) raw[k] = gload_at<NT>(src + (w * C + k) * 512, ld_off);
   }
-  wave_stages<kMfma, L, C, kDual>(v, lane);
+  wave_stages<kMfma, L, C>(v, lane);
   exchange_wave_bits<C, NW, HALVES>(v, lds, w, lane, true);
-  const int lf = lane_field<kMfma, L, kDual>(lane);
+  const int lf = lane_field<kMfma, L>(lane);
   if constexpr (EPI == kStore16) {
     const Finisher<DT, kMfma> fin(twisted<kMfma, L>(lane), sc.post);
     uint16_t *dst = out + row * out_stride;
@@ -1012,21 +1019,16 @@ __device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16
     for (int i = 1; i < NW; ++i) a = fmaxf(a, wave_max[i]);
     const RowQuant<kMfma, EPI> qz(a, twisted<kMfma, L>(lane), sc.post, lane);
     uint8_t *codes = qo.codes + row * qo.stride;
+    const uint16_t *src = in + (more ? next : m - 1) * in_stride;
+    const uint32_t ld_off = (uint32_t)(lane_field_load<kMfma, L>(lane) * 16);
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const int W = (k % NW) * C + (k / NW) * NW + w;
       gstore8_at<NT>(codes + W * 512, (uint32_t)(lf * 8), qz.codes(&v[k * 8]));
+      // the chunks not prefetched yet go out as stored chunks free registers
+      if (k < C - PRE) raw[PRE + k] = gload_at<NT>(src + (w * C + PRE + k) * 512, ld_off);
     }
     if (threadIdx.x == 0) qo.scales[row] = qz.scale;
-  }
-  if constexpr (PRE < C) {
-    if (more) {
-      __builtin_amdgcn_sched_barrier(0);
-      const uint16_t *src = in + next * in_stride;
-      const uint32_t ld_off = (uint32_t)(lane_field_load<kMfma, L>(lane) * 16);
-#pragma unroll
-      for (int k = PRE; k < C; ++k) raw[k] = gload_at<NT>(src + (w * C + k) * 512, ld_off);
-    }
   }
   return more;
 }
@@ -1035,7 +1037,7 @@ template <int DT, int L, int C, int HALVES, bool NT, int EPI>
 __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_loop_kernel(
     const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc,
     QuantOut qo, int64_t m) {
-  constexpr int PRE = EPI == kStore16 ? C : 12;
+  constexpr int PRE = EPI == kStore16 ? C : 14;
   __shared__ float4 lds[(1 << L) / 4 / HALVES];
   __shared__ float wave_max[(1 << L) / (512 * C)];
   const int lane = threadIdx.x & (kWave - 1);
