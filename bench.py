@@ -202,6 +202,18 @@ def time_workload(d: Device, w, steps: int, warmup: int, min_warm_s: float = 0.0
     }
 
 
+# The paper's own performance claims (abstract; §5): speedups of its CUDA kernel
+# over the Dao AI Lab fast-hadamard-transform kernel, fp16, n = 2^7 ... 2^15, on
+# other hardware.  Context only: they are ratios between two kernels on A100 and
+# H100, not a rate on this GPU, so vs_baseline stays null.
+PAPER_CONTEXT = {
+    "kind": "speedup over the paper's baseline FWHT kernel, other hardware, context only",
+    "a100_pcie": {"typical": "1.1-1.4x", "peak": "3.5x"},
+    "h100_pcie": {"typical": "1.0-1.3x", "peak": "3.6x"},
+    "source": "abstract and Sec. 5",
+}
+
+
 def cpu_baseline(w, target_seconds: float, quant: str | None = None) -> dict:
     """The fp64 oracle on the host cores, timed on a bounded row sample of the workload
     (with quant, the oracle's fused transform + quantization, which runs on one thread)."""
@@ -297,6 +309,7 @@ def main(argv=None) -> int:
             "bound": "hbm", "achieved": r["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": r["frac_hbm_peak"], "traffic": traffic,
         },
+        "paper_context": PAPER_CONTEXT,
     }
     if args.sweep:
         from paper_2412_08832_amd import workloads as W

@@ -1,0 +1,77 @@
+"""Host logic of bench.py, checked on the CPU: the one-GPU rule, workload names,
+the traffic figure read from the committed rocprofv3 summaries, and the
+paper-context object of the JSON line."""
+from __future__ import annotations
+
+import re
+import subprocess
+import sys
+
+import pytest
+
+import bench
+from paper_2412_08832_amd import workloads as W
+
+
+def _profile_fields(path):
+    return dict(re.findall(r"^([a-z_0-9]+):\s*(\S+)\s*$", path.read_text(), flags=re.M))
+
+
+PROFILES = sorted(bench.PROFILES.glob("*.txt"))
+
+
+def test_more_than_one_gpu_exits_with_a_message():
+    res = subprocess.run([sys.executable, str(bench.ROOT / "bench.py"), "--gpus", "2"],
+                         capture_output=True, text=True, timeout=120)
+    assert res.returncode == 2
+    assert "one GPU" in res.stderr
+    assert res.stdout == ""
+
+
+def test_workload_names():
+    w = bench.workload_by_name("sweep:bf16:16:in")
+    assert (w.n, w.m, w.dtype, w.inplace) == (65536, 4096, "bf16", True)
+    w = bench.workload_by_name("sweep:fp16:7:out")
+    assert (w.n, w.m, w.dtype, w.inplace) == (128, 1 << 21, "fp16", False)
+    assert bench.workload_by_name("bf16_1048576x128_inplace") is W.WORKLOADS["bf16_1048576x128_inplace"]
+    with pytest.raises(SystemExit):
+        bench.workload_by_name("sweep:fp32:7:in")
+
+
+def test_default_workload_is_the_headline_configuration():
+    args = bench.parse_args([])
+    w = bench.workload_by_name(args.workload)
+    assert (w.m, w.n, w.dtype, w.inplace) == (1048576, 128, "bf16", True)
+    assert args.gpus == 1
+
+
+@pytest.mark.parametrize("path", PROFILES, ids=[p.stem for p in PROFILES])
+def test_profile_summary_is_consistent(path):
+    """Each summary names its command, and its figures agree with each other:
+    achieved GB/s = algorithmic bytes / average duration, and the counted HBM
+    traffic is within 1% of the algorithmic bytes (no re-reads)."""
+    f = _profile_fields(path)
+    text = path.read_text()
+    assert "rocprofv3" in text and "bench.py" in text
+    assert re.fullmatch(r"[0-9a-f]{64}", f["source_sha256"])
+    alg = float(f["algorithmic_bytes_per_launch"])
+    avg = float(f["kernel_avg_ns_last_200_calls"])
+    assert float(f["achieved_gbs_last_200_calls"]) == pytest.approx(alg / avg, rel=2e-3)
+    if "traffic_bytes_per_launch" in f:
+        assert float(f["traffic_bytes_per_launch"]) / alg == pytest.approx(1.0, abs=0.01)
+
+
+@pytest.mark.parametrize("path", [p for p in PROFILES if "traffic_bytes_per_launch" in
+                                  _profile_fields(p)], ids=lambda p: p.stem)
+def test_traffic_is_read_only_for_the_profiled_source(path):
+    f = _profile_fields(path)
+    got = bench.measured_traffic(f["workload"], f["source_sha256"])
+    assert got == int(float(f["traffic_bytes_per_launch"]))
+    assert bench.measured_traffic(f["workload"], "0" * 64) is None
+
+
+def test_paper_context_is_context_only():
+    ctx = bench.PAPER_CONTEXT
+    assert ctx["a100_pcie"] == {"typical": "1.1-1.4x", "peak": "3.5x"}
+    assert ctx["h100_pcie"] == {"typical": "1.0-1.3x", "peak": "3.6x"}
+    assert "context" in ctx["kind"]
