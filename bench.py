@@ -251,6 +251,13 @@ def cpu_baseline(w, target_seconds: float, quant: str | None = None) -> dict:
         sec = time.perf_counter() - t0
         if sec >= target_seconds or passes >= 1000:
             break
+    single = None
+    if not quant and cores > 1:
+        # the same oracle on one thread, over a sample sized for ~1/4 of the target
+        rows1 = max(1, min(rows, int(rows * passes / cores / 4)))
+        t1 = time.perf_counter()
+        orc.fwht(np.ascontiguousarray(bits[:rows1]), w.dtype, w.scale, nthreads=1)
+        single = rows1 * w.n / max(time.perf_counter() - t1, 1e-6)
     cpu = ""
     try:
         for line in Path("/proc/cpuinfo").read_text().splitlines():
@@ -259,13 +266,16 @@ def cpu_baseline(w, target_seconds: float, quant: str | None = None) -> dict:
                 break
     except OSError:
         pass
-    return {
+    out = {
         "value": passes * rows * w.n / sec, "unit": "elements/s", "cores": cores, "kind": "oracle",
         "sample": f"{passes} pass(es) over the first {rows} of {w.m} rows ({rows * w.n} "
                   f"elements each), {sec:.1f} s, "
                   + (f"fp64 iterative FWHT + {quant} quantization in C on 1 thread, " if quant
                      else f"fp64 iterative FWHT in C on {cores} threads, ") + cpu,
     }
+    if single is not None:
+        out["value_1_thread"] = single
+    return out
 
 
 def main(argv=None) -> int:

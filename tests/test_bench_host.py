@@ -75,3 +75,16 @@ def test_paper_context_is_context_only():
     assert ctx["a100_pcie"] == {"typical": "1.1-1.4x", "peak": "3.5x"}
     assert ctx["h100_pcie"] == {"typical": "1.0-1.3x", "peak": "3.6x"}
     assert "context" in ctx["kind"]
+
+
+def test_cpu_baseline_fields():
+    """The oracle baseline on a small workload: the contract's fields, plus the
+    one-thread rate when more than one core is used."""
+    r = bench.cpu_baseline(W.WORKLOADS["fp16_1024x256"], 0.2)
+    assert r["kind"] == "oracle" and r["unit"] == "elements/s"
+    assert r["value"] > 0 and r["cores"] >= 1
+    assert "pass(es) over the first" in r["sample"]
+    if r["cores"] > 1:
+        assert r["value_1_thread"] > 0
+    q = bench.cpu_baseline(W.WORKLOADS["fp16_1024x256"], 0.2, quant="fp8")
+    assert q["cores"] == 1 and "value_1_thread" not in q
