@@ -110,3 +110,109 @@ def test_concurrent_streams_match_serial():
                                  s2.cuda_stream)
         torch.cuda.synchronize()
         assert torch.equal(oa, ra) and torch.equal(ob, rb)
+
+
+def test_host_threads_match_serial():
+    """Calls from four host threads at once, each on its own stream and buffers
+    (wave kernel, block kernel, persistent loop, FP8 output), give the same bits
+    as the same calls made one after the other from one thread."""
+    import threading
+    import torch
+    gen = torch.Generator(device="cuda").manual_seed(11)
+    jobs = [  # (m, n, torch dtype, library dtype, fp8 output)
+        (8192, 4096, torch.bfloat16, H.BF16, False),
+        (1 << 16, 128, torch.float16, H.FP16, False),
+        (300, 1 << 16, torch.bfloat16, H.BF16, False),
+        (4096, 1024, torch.float16, H.FP16, True),
+    ]
+    xs = [torch.randn(m, n, device="cuda", generator=gen).to(dt) for m, n, dt, _, _ in jobs]
+
+    def outputs(i):
+        m, n, dt, _, q = jobs[i]
+        if q:
+            return (torch.empty(m, n, dtype=torch.uint8, device="cuda"),
+                    torch.empty(m, dtype=torch.float32, device="cuda"))
+        return (torch.empty(m, n, dtype=dt, device="cuda"),)
+
+    def call(i, outs, stream):
+        m, n, _, code, q = jobs[i]
+        x = xs[i]
+        if q:
+            H.hadamard_transform_fp8(x.data_ptr(), n, outs[0].data_ptr(), n, outs[1].data_ptr(),
+                                     m, n, code, n ** -0.5, stream)
+        else:
+            H.hadamard_transform(x.data_ptr(), outs[0].data_ptr(), m, n, code, n ** -0.5, stream)
+
+    s0 = torch.cuda.current_stream().cuda_stream
+    refs = [outputs(i) for i in range(len(jobs))]
+    for i in range(len(jobs)):
+        call(i, refs[i], s0)
+    torch.cuda.synchronize()
+
+    streams = [torch.cuda.Stream() for _ in jobs]
+    for _ in range(2):
+        got = [outputs(i) for i in range(len(jobs))]
+        for o in got:
+            for t in o:
+                t.zero_()
+        torch.cuda.synchronize()
+        errors = []
+        start = threading.Barrier(len(jobs))
+
+        def worker(i):
+            try:
+                start.wait()
+                for _ in range(5):
+                    call(i, got[i], streams[i].cuda_stream)
+            except Exception as e:  # reported below, in the main thread
+                errors.append(e)
+
+        threads = [threading.Thread(target=worker, args=(i,)) for i in range(len(jobs))]
+        for t in threads:
+            t.start()
+        for t in threads:
+            t.join(timeout=120)
+        assert not any(t.is_alive() for t in threads), "a host thread did not finish"
+        assert not errors, errors
+        torch.cuda.synchronize()
+        for i in range(len(jobs)):
+            for a, b in zip(got[i], refs[i]):
+                assert torch.equal(a, b), f"job {i} differs from the serial result"
+
+
+def test_graph_replays_two_pass_size():
+    """n = 2^17 runs two kernels through the caller's workspace; captured and
+    replayed, each replay equals the eager call on the same input."""
+    import torch
+    m, n = 24, 1 << 17
+    gen = torch.Generator(device="cuda").manual_seed(17)
+    x = torch.empty(m, n, dtype=torch.bfloat16, device="cuda")
+    out = torch.empty_like(x)
+    ws = torch.empty(H.hadamard_transform_workspace_size(m, n), dtype=torch.uint8, device="cuda")
+
+    def enqueue(stream):
+        H.hadamard_transform_ws(x.data_ptr(), n, out.data_ptr(), n, m, n, H.BF16, n ** -0.5,
+                                ws.data_ptr(), ws.numel(), stream)
+
+    x.copy_(torch.randn(m, n, device="cuda", generator=gen).to(torch.bfloat16))
+    enqueue(torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            enqueue(side.cuda_stream)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for replay in range(3):
+        x.copy_(torch.randn(m, n, device="cuda", generator=gen).to(torch.bfloat16))
+        enqueue(torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        ref = out.clone()
+        out.zero_()
+        ws.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), f"replay {replay}: two-pass transform differs from eager"
