@@ -884,6 +884,13 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   const int lane = threadIdx.x & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   const int64_t row = blockIdx.x;
+  // The waves run at raised priority until their front end is done, so a
+  // workgroup that has just started (its loads, then the first stages on
+  // them) goes ahead of the in-wave stages of the workgroup already resident
+  // on the CU.  Measured: +2% at n = 32768, +1-3% for FP8 at n = 8192 and
+  // 16384, neutral below; raising it for the exchange or the stores instead,
+  // or dropping it before the front end, was neutral or slower.
+  if constexpr (!IN32) __builtin_amdgcn_s_setprio(3);
 
   float v[C * 8];
   if constexpr (IN32) {
@@ -915,6 +922,7 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
       raw[k] = gload_at<NT>(src, (uint32_t)(((w * C + k) * kWave + lf_load) * 16));
     }
     front<DT, FRONT, C>(raw, v, lane, sc.scale, sc.e2);
+    __builtin_amdgcn_s_setprio(0);
   }
   wave_stages<FRONT, L, C>(v, lane);
   exchange_wave_bits<C, NW, HALVES>(v, lds, w, lane, false);
