@@ -887,10 +887,13 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   // The waves run at raised priority until their front end is done, so a
   // workgroup that has just started (its loads, then the first stages on
   // them) goes ahead of the in-wave stages of the workgroup already resident
-  // on the CU.  Measured: +2% at n = 32768, +1-3% for FP8 at n = 8192 and
-  // 16384, neutral below; raising it for the exchange or the stores instead,
-  // or dropping it before the front end, was neutral or slower.
-  if constexpr (!IN32) __builtin_amdgcn_s_setprio(3);
+  // on the CU.  Measured against the same kernel without it, n = 8192-32768:
+  // bf16 input +0.4-3.7%, FP8/INT8 output +0-4.1%; fp16 input with 16-bit
+  // output -0.4-3.5%, so that case keeps the default priority.  Raising it for
+  // the exchange or the stores instead, or dropping it before the front end,
+  // was neutral or slower.
+  constexpr bool kRaise = !IN32 && !(EPI == kStore16 && DT == HADACORE_FP16);
+  if constexpr (kRaise) __builtin_amdgcn_s_setprio(3);
 
   float v[C * 8];
   if constexpr (IN32) {
@@ -922,7 +925,7 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
       raw[k] = gload_at<NT>(src, (uint32_t)(((w * C + k) * kWave + lf_load) * 16));
     }
     front<DT, FRONT, C>(raw, v, lane, sc.scale, sc.e2);
-    __builtin_amdgcn_s_setprio(0);
+    if constexpr (kRaise) __builtin_amdgcn_s_setprio(0);
   }
   wave_stages<FRONT, L, C>(v, lane);
   exchange_wave_bits<C, NW, HALVES>(v, lds, w, lane, false);
