@@ -137,6 +137,42 @@ def test_int8_n65536_several_rows_per_workgroup(oracle, dtype, variant):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
+def test_int8_n65536_special_rows_between_ordinary_rows(oracle, dtype, variant):
+    """The persistent n = 65536 kernel carries a workgroup from row r to row
+    r + CUs: zero, NaN and Inf rows before and after ordinary rows of the same
+    workgroup must leave no trace in the rows that follow (row maximum, scale,
+    cleared codes)."""
+    import torch
+    n = 1 << 16
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    m = 2 * cus + 5
+    say(f"int8 n=65536 special rows m={m} {dtype} variant={variant}")
+    bits = W.random_rows(m, n, dtype, seed=66)
+    nan = 0x7E00 if dtype == "fp16" else 0x7FC0
+    inf = 0x7C00 if dtype == "fp16" else 0x7F80
+    zero_rows = [0, cus + 5, 2 * cus + 2]
+    nan_rows = [1, cus + 6]
+    inf_rows = [2, 2 * cus + 1]
+    for r in zero_rows:
+        bits[r] = 0
+    for r in nan_rows:
+        bits[r, (7 * r) % n] = nan
+    for r in inf_rows:
+        bits[r, (3 * r) % n] = inf
+    s = W.default_scale(n)
+    codes, scales = _run_int8(bits, dtype, s, n)
+    for r in zero_rows:
+        assert scales[r] == 0 and np.all(codes[r] == 0), r
+    for r in nan_rows:
+        assert np.isnan(scales[r]) and np.all(codes[r] == 0), r
+    for r in inf_rows:
+        assert np.isinf(scales[r]) and np.all(codes[r] == 0), r
+    c = compare_int8(oracle, codes, scales, bits, dtype, s, n)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", [0, 1, 2, 3, 5, 7, 12, 15, 16])
 def test_int8_special_rows(oracle, L, dtype, variant):
     n = 1 << L
