@@ -134,6 +134,32 @@ def test_n65536_several_rows_per_workgroup(oracle, dtype, inplace, variant):
     assert c.ok, str(c)
 
 
+@pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_n65536_nonfinite_rows_between_ordinary_rows(oracle, dtype, inplace, variant):
+    """NaN, Inf and zero rows handled by a persistent n = 65536 workgroup before
+    and after ordinary rows: nothing carries over to the rows that follow."""
+    import torch
+    n = 1 << 16
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    m = 2 * cus + 5
+    say(f"n=65536 nonfinite rows m={m} {dtype} inplace={inplace} variant={variant}")
+    bits = W.random_rows(m, n, dtype, seed=67)
+    nan = 0x7E00 if dtype == "fp16" else 0x7FC0
+    inf = 0x7C00 if dtype == "fp16" else 0x7F80
+    bits[0, 11] = nan
+    bits[cus + 1, 5] = nan
+    bits[1, 3] = inf
+    bits[2 * cus, 1] = inf | 0x8000
+    bits[2] = 0
+    bits[cus + 3] = 0
+    s = W.default_scale(n)
+    out = _run(bits, dtype, s, n, inplace)
+    c = compare_with_oracle(oracle, out, bits, dtype, s, n)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
 # scales beyond 1/sqrt(n): zero, negative, not a power of two, far from 1 (kept
 # where the outputs stay inside the dtype's range, so that the comparison with
 # the unrounded oracle is meaningful)
