@@ -173,7 +173,7 @@ def test_int8_n65536_special_rows_between_ordinary_rows(oracle, dtype, variant):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [0, 1, 2, 3, 5, 7, 12, 15, 16])
+@pytest.mark.parametrize("L", [0, 1, 2, 3, 5, 7, 8, 9, 12, 15, 16])
 def test_int8_special_rows(oracle, L, dtype, variant):
     n = 1 << L
     bits = W.random_rows(6, n, dtype, seed=9)
