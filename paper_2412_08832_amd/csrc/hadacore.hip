@@ -1406,6 +1406,9 @@ hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int6
 }
 
 // Launch configuration of one (size, epilogue, front end).
+// Row count from which n = 32768 (bf16) takes its long-call shape.
+constexpr int64_t kLongCallRows = 8192;
+
 struct Cfg {
   int C;       // chunks of 8 elements per lane
   int T;       // tiles per wave (wave kernel)
@@ -1471,6 +1474,15 @@ template <int DT, int L, int EPI, int FRONT>
 hipError_t launch_front(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
                         int64_t m, const ScaleArgs &sc, hipStream_t stream, QuantOut qo) {
   constexpr Cfg c = config<L, EPI, FRONT>();
+  if constexpr (L == 15 && EPI == kStore16 && FRONT == kMfma && DT == HADACORE_BF16) {
+    // n = 32768, bf16: from 8192 rows, 4 waves of 16 chunks per row beat 8
+    // waves of 8 (+1-3.5% up to 16384 rows).  Below, their longer-lived
+    // workgroups weigh more at the start and end of the call: -3% at 4096
+    // rows, -8% at 2048, even at 6144.
+    if (m >= kLongCallRows)
+      return launch_cfg<DT, L, 16, 1, 1, 2, FRONT, EPI>(in, in_stride, out, out_stride, m, sc,
+                                                        stream, qo);
+  }
   return launch_cfg<DT, L, c.C, c.T, c.WPB, c.HALVES, FRONT, EPI>(in, in_stride, out, out_stride,
                                                                   m, sc, stream, qo);
 }

@@ -160,6 +160,23 @@ def test_n65536_nonfinite_rows_between_ordinary_rows(oracle, dtype, inplace, var
     assert c.ok, str(c)
 
 
+@pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])
+@pytest.mark.parametrize("m", [8191, 8192])
+def test_n32768_bf16_either_side_of_the_long_call_shape(oracle, m, inplace):
+    """bf16 n = 32768 switches to 16 chunks per lane from 8192 rows; both sides
+    of the switch against the oracle on sampled rows (first, last, random)."""
+    n = 1 << 15
+    say(f"bf16 n=32768 m={m} inplace={inplace}")
+    bits = W.random_rows(m, n, "bf16", seed=m)
+    s = W.default_scale(n)
+    out = _run(bits, "bf16", s, n, inplace)
+    rng = np.random.default_rng(m)
+    rows = np.unique(np.r_[0, 1, m - 2, m - 1, rng.integers(0, m, 128)])
+    c = compare_with_oracle(oracle, out, bits, "bf16", s, n, rows=rows)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
 # scales beyond 1/sqrt(n): zero, negative, not a power of two, far from 1 (kept
 # where the outputs stay inside the dtype's range, so that the comparison with
 # the unrounded oracle is meaningful)
