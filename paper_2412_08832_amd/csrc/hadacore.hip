@@ -1306,11 +1306,24 @@ __global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uin
     const int64_t i0 = base >> L;
     float w[8];
     uint32_t keep[2] = {0u, 0u};
+    float sc8[8 / N];
 #pragma unroll
     for (int r = 0; r < 8 / N; ++r) {
       float amax = fabsf(v[r * N]);
 #pragma unroll
       for (int j = 1; j < N; ++j) amax = fmaxf(amax, fabsf(v[r * N + j]));
+      if constexpr (N == 1) {
+        // A one-element row: wherever Q / amax is finite, RN(Q / amax) * v lies
+        // within 2^-23 of +-Q, which both conversions map to the largest code
+        // of v's sign, so that code is written without the quotient.  Codes,
+        // scale and mask are those of the general path below.
+        if (amax >= 0x1p-100f && amax < __builtin_inff()) {
+          w[r] = __builtin_copysignf(EPI == kFp8 ? 448.0f : 127.0f, v[r]);
+          keep[r / 4] |= 0xFFu << (8 * (r % 4));
+          sc8[r] = RowQuant<kValu, EPI>::div_by_q(amax);
+          continue;
+        }
+      }
       const RowQuant<kValu, EPI> qz(amax);
 #pragma unroll
       for (int j = 0; j < N; ++j) w[r * N + j] = v[r * N + j] * qz.mul;
@@ -1320,7 +1333,18 @@ __global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uin
         const int b = r * N + j;
         keep[b / 4] |= (qz.keep & 0xFFu) << (8 * (b % 4));
       }
-      if (r * N < count) qo.scales[i0 + r] = qz.scale;
+      sc8[r] = qz.scale;
+    }
+    if (count == 8 && N <= 2 && (reinterpret_cast<uintptr_t>(qo.scales) & 15) == 0) {
+      // 8 / N consecutive row scales at a 16-byte boundary (i0 is a multiple of
+      // 8 / N); a scales array that is only 4-byte aligned takes the loop below
+#pragma unroll
+      for (int q = 0; q < 8 / N; q += 4)
+        *reinterpret_cast<f4 *>(qo.scales + i0 + q) = f4{sc8[q], sc8[q + 1], sc8[q + 2], sc8[q + 3]};
+    } else {
+#pragma unroll
+      for (int r = 0; r < 8 / N; ++r)
+        if (r * N < count) qo.scales[i0 + r] = sc8[r];
     }
     const u2 raw = EPI == kFp8 ? to_e4m3x8(w, 1.0f) : to_int8x8(w, 1.0f, 0xFFFFFFFFu);
     const u2 c = EPI == kFp8 ? raw : u2{raw.x & keep[0], raw.y & keep[1]};

@@ -135,6 +135,33 @@ def test_fp8_n65536_several_rows_per_workgroup(oracle, dtype, variant):
     assert c.ok, str(c)
 
 
+@pytest.mark.parametrize("L", [0, 1, 2])
+def test_fp8_scales_only_4_byte_aligned(oracle, L):
+    """The scales array need only be 4-byte aligned.  For n <= 2 the kernel
+    stores 8 / n scales at once when the array is 16-byte aligned, one at a
+    time otherwise: both give the same bits, and match the oracle."""
+    import torch
+    n = 1 << L
+    m = 4099
+    bits = W.random_rows(m, n, "bf16", seed=40 + L)
+    s = W.default_scale(n)
+    x = to_device(bits, "bf16")
+    got = []
+    for off in (0, 1):
+        codes = torch.zeros((m, n), dtype=torch.uint8, device="cuda")
+        buf = torch.full((m + 4,), -1.0, dtype=torch.float32, device="cuda")
+        H.hadamard_transform_fp8(x.data_ptr(), n, codes.data_ptr(), n, buf.data_ptr() + 4 * off,
+                                   m, n, H.BF16, s, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        b = buf.cpu().numpy()
+        assert b[off - 1 if off else m] == -1.0 and b[off + m] == -1.0, "write outside the scales"
+        got.append((codes.cpu().numpy(), b[off:off + m].copy()))
+    assert np.array_equal(got[0][0], got[1][0])
+    assert np.array_equal(got[0][1].view(np.int32), got[1][1].view(np.int32))
+    c = compare_fp8(oracle, got[1][0], got[1][1], bits, "bf16", s, n)
+    assert c.ok, str(c)
+
+
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_fp8_n65536_special_rows_between_ordinary_rows(oracle, dtype, variant):
     """The persistent n = 65536 kernel carries a workgroup from row r to row
