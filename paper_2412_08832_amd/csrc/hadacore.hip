@@ -1335,12 +1335,18 @@ __global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uin
       }
       sc8[r] = qz.scale;
     }
-    if (count == 8 && N <= 2 && (reinterpret_cast<uintptr_t>(qo.scales) & 15) == 0) {
-      // 8 / N consecutive row scales at a 16-byte boundary (i0 is a multiple of
-      // 8 / N); a scales array that is only 4-byte aligned takes the loop below
+    // 8 / N consecutive row scales, at a multiple of 8 / N (i0 is one): 16-byte
+    // stores for n <= 2, one 8-byte store for n = 4, when the scales array is
+    // aligned for them; a scales array that is only 4-byte aligned takes the loop
+    constexpr uintptr_t kAlign = N <= 2 ? 15 : 7;
+    if (count == 8 && N <= 4 && (reinterpret_cast<uintptr_t>(qo.scales) & kAlign) == 0) {
+      if constexpr (N <= 2) {
 #pragma unroll
-      for (int q = 0; q < 8 / N; q += 4)
-        *reinterpret_cast<f4 *>(qo.scales + i0 + q) = f4{sc8[q], sc8[q + 1], sc8[q + 2], sc8[q + 3]};
+        for (int q = 0; q < 8 / N; q += 4)
+          *reinterpret_cast<f4 *>(qo.scales + i0 + q) = f4{sc8[q], sc8[q + 1], sc8[q + 2], sc8[q + 3]};
+      } else {
+        *reinterpret_cast<f2 *>(qo.scales + i0) = f2{sc8[0], sc8[1]};
+      }
     } else {
 #pragma unroll
       for (int r = 0; r < 8 / N; ++r)
