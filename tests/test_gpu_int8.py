@@ -225,7 +225,7 @@ def test_int8_special_rows(oracle, L, dtype, variant):
     assert c.ok, str(c)
 
 
-@pytest.mark.parametrize("L", [2, 5, 7, 9, 13, 16])
+@pytest.mark.parametrize("L", [0, 1, 2, 5, 7, 9, 13, 16])
 def test_int8_strided_codes_keep_gaps(oracle, L, variant):
     n = 1 << L
     m = 13

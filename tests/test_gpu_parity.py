@@ -216,7 +216,7 @@ def test_zero_rows_leaves_output_untouched():
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("L", [1, 3, 5, 7, 9, 12, 14, 16])
+@pytest.mark.parametrize("L", [0, 1, 2, 3, 5, 7, 9, 12, 14, 16])
 def test_strided_rows_keep_gaps(oracle, L, dtype, variant):
     n = 1 << L
     m = 19
