@@ -17,7 +17,9 @@ def _profile_fields(path):
     return dict(re.findall(r"^([a-z_0-9]+):\s*(\S+)\s*$", path.read_text(), flags=re.M))
 
 
-PROFILES = sorted(bench.PROFILES.glob("*.txt"))
+PROFILES = sorted(p for p in bench.PROFILES.glob("*.txt")
+                  if "algorithmic_bytes_per_launch" in _profile_fields(p))
+COUNTER_SUMMARIES = sorted(p for p in bench.PROFILES.glob("*.txt") if p not in PROFILES)
 
 
 def test_more_than_one_gpu_exits_with_a_message():
@@ -68,6 +70,23 @@ def test_traffic_is_read_only_for_the_profiled_source(path):
     got = bench.measured_traffic(f["workload"], f["source_sha256"])
     assert got == int(float(f["traffic_bytes_per_launch"]))
     assert bench.measured_traffic(f["workload"], "0" * 64) is None
+
+
+@pytest.mark.parametrize("path", COUNTER_SUMMARIES, ids=[p.stem for p in COUNTER_SUMMARIES])
+def test_counter_summary_names_its_command_and_source(path):
+    """Counter-only summaries (no timing) name the rocprofv3 command, the source
+    they were taken on and per-kernel shares between 0 and 1."""
+    text = path.read_text()
+    f = _profile_fields(path)
+    assert "rocprofv3 --pmc" in text and "bench.py" in text
+    assert re.fullmatch(r"[0-9a-f]{64}", f["source_sha256"])
+    shares = [float(v) for k, v in re.findall(r"^([a-z_]+_share):\s*(\S+)$", text, flags=re.M)]
+    assert shares and all(0.0 <= x <= 1.0 for x in shares)
+
+
+def test_every_summary_is_checked():
+    assert len(PROFILES) + len(COUNTER_SUMMARIES) == len(list(bench.PROFILES.glob("*.txt")))
+    assert PROFILES, "no kernel-trace summaries"
 
 
 def test_paper_context_is_context_only():
