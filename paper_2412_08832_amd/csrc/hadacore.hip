@@ -1436,8 +1436,9 @@ hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int6
 }
 
 // Launch configuration of one (size, epilogue, front end).
-// Row count from which n = 32768 (bf16) takes its long-call shape.
-constexpr int64_t kLongCallRows = 8192;
+// Row counts from which n = 32768 takes its long-call shape (bf16, fp16).
+constexpr int64_t kLongCallRowsBf16 = 8192;
+constexpr int64_t kLongCallRowsFp16 = 12288;
 
 struct Cfg {
   int C;       // chunks of 8 elements per lane
@@ -1504,12 +1505,12 @@ template <int DT, int L, int EPI, int FRONT>
 hipError_t launch_front(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
                         int64_t m, const ScaleArgs &sc, hipStream_t stream, QuantOut qo) {
   constexpr Cfg c = config<L, EPI, FRONT>();
-  if constexpr (L == 15 && EPI == kStore16 && FRONT == kMfma && DT == HADACORE_BF16) {
-    // n = 32768, bf16: from 8192 rows, 4 waves of 16 chunks per row beat 8
-    // waves of 8 (+1-3.5% up to 16384 rows).  Below, their longer-lived
-    // workgroups weigh more at the start and end of the call: -3% at 4096
-    // rows, -8% at 2048, even at 6144.
-    if (m >= kLongCallRows)
+  if constexpr (L == 15 && EPI == kStore16 && FRONT == kMfma) {
+    // n = 32768: from enough rows, 4 waves of 16 chunks per row beat 8 waves
+    // of 8 (bf16 from 8192 rows: +1-3.5%; fp16 from 12288: +0.2-4.4%).  Below,
+    // their longer-lived workgroups weigh more at the start and end of the
+    // call: bf16 -3% at 4096 rows and -8% at 2048, fp16 mixed at 8192.
+    if (m >= (DT == HADACORE_BF16 ? kLongCallRowsBf16 : kLongCallRowsFp16))
       return launch_cfg<DT, L, 16, 1, 1, 2, FRONT, EPI>(in, in_stride, out, out_stride, m, sc,
                                                         stream, qo);
   }

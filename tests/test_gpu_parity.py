@@ -161,18 +161,19 @@ def test_n65536_nonfinite_rows_between_ordinary_rows(oracle, dtype, inplace, var
 
 
 @pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])
-@pytest.mark.parametrize("m", [8191, 8192])
-def test_n32768_bf16_either_side_of_the_long_call_shape(oracle, m, inplace):
-    """bf16 n = 32768 switches to 16 chunks per lane from 8192 rows; both sides
-    of the switch against the oracle on sampled rows (first, last, random)."""
+@pytest.mark.parametrize("dtype,m", [("bf16", 8191), ("bf16", 8192), ("fp16", 12287), ("fp16", 12288)])
+def test_n32768_either_side_of_the_long_call_shape(oracle, dtype, m, inplace):
+    """n = 32768 switches to 16 chunks per lane from 8192 rows (bf16) or 12288
+    rows (fp16); both sides of each switch against the oracle on sampled rows
+    (first, last, random)."""
     n = 1 << 15
-    say(f"bf16 n=32768 m={m} inplace={inplace}")
-    bits = W.random_rows(m, n, "bf16", seed=m)
+    say(f"{dtype} n=32768 m={m} inplace={inplace}")
+    bits = W.random_rows(m, n, dtype, seed=m)
     s = W.default_scale(n)
-    out = _run(bits, "bf16", s, n, inplace)
+    out = _run(bits, dtype, s, n, inplace)
     rng = np.random.default_rng(m)
     rows = np.unique(np.r_[0, 1, m - 2, m - 1, rng.integers(0, m, 128)])
-    c = compare_with_oracle(oracle, out, bits, "bf16", s, n, rows=rows)
+    c = compare_with_oracle(oracle, out, bits, dtype, s, n, rows=rows)
     say(f"  {c}")
     assert c.ok, str(c)
 
