@@ -52,6 +52,11 @@
  * (testing and tuning; read on every call); unset keeps the measured per-size
  * choice.
  *
+ * Launches: a call is one kernel launch, or two for the two-pass sizes; m so
+ * large that a launch would exceed 2^31 work-items (2^33 elements) is split
+ * into several launches of consecutive rows on the same stream, with the
+ * same result.
+ *
  * Errors: arguments are validated synchronously before anything is enqueued;
  * on error nothing is enqueued and a nonzero status is returned.  No call
  * aborts or throws.  The library keeps no state beyond a per-device cache of
@@ -67,7 +72,7 @@
 extern "C" {
 #endif
 
-#define HADACORE_VERSION 10100 /* 1.1.0: one-pass n = 2^16 */
+#define HADACORE_VERSION 10101 /* 1.1.1: very large m split over launches */
 
 typedef int32_t hadacore_dtype;
 #define HADACORE_FP16 0 /* IEEE binary16 */
@@ -83,7 +88,7 @@ typedef int32_t hadacore_status;
 #define HADACORE_ERROR_OVERLAP 6            /* in/out overlap without being the same layout */
 #define HADACORE_ERROR_LAUNCH 7             /* the HIP runtime rejected the kernel launch */
 #define HADACORE_ERROR_UNSUPPORTED_DEVICE 8 /* current device is not gfx950 */
-#define HADACORE_ERROR_TOO_LARGE 9          /* m too large for one launch (m >= 2^31) */
+#define HADACORE_ERROR_TOO_LARGE 9          /* m >= 2^31, or m * row stride > 2^40 */
 #define HADACORE_ERROR_WORKSPACE 10         /* workspace NULL or below the required size */
 
 /*

@@ -1533,10 +1533,10 @@ hipError_t launch(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t 
   }
 }
 
-template <int DT, int EPI = kStore16>
-hipError_t launch_dt(int L, const uint16_t *in, int64_t in_stride, uint16_t *out,
-                     int64_t out_stride, int64_t m, const ScaleArgs &sc, int front,
-                     hipStream_t stream, QuantOut qo = {}) {
+template <int DT, int EPI>
+hipError_t launch_dt_one(int L, const uint16_t *in, int64_t in_stride, uint16_t *out,
+                         int64_t out_stride, int64_t m, const ScaleArgs &sc, int front,
+                         hipStream_t stream, QuantOut qo) {
   switch (L) {
     case 0: return launch<DT, 0, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
     case 1: return launch<DT, 1, EPI>(in, in_stride, out, out_stride, m, sc, front, stream, qo);
@@ -1583,9 +1583,9 @@ hipError_t launch_large(const uint16_t *in, int64_t in_stride, uint16_t *out, in
 }
 
 template <int DT>
-hipError_t launch_large_dt(int L, const uint16_t *in, int64_t in_stride, uint16_t *out,
-                           int64_t out_stride, int64_t m, float scale, float *ws,
-                           hipStream_t stream) {
+hipError_t launch_large_one(int L, const uint16_t *in, int64_t in_stride, uint16_t *out,
+                            int64_t out_stride, int64_t m, float scale, float *ws,
+                            hipStream_t stream) {
   switch (L) {
     case 17: return launch_large<DT, 4>(in, in_stride, out, out_stride, m, scale, ws, stream);
     case 18: return launch_large<DT, 8>(in, in_stride, out, out_stride, m, scale, ws, stream);
@@ -1593,6 +1593,57 @@ hipError_t launch_large_dt(int L, const uint16_t *in, int64_t in_stride, uint16_
     case 20: return launch_large<DT, 32>(in, in_stride, out, out_stride, m, scale, ws, stream);
     default: return hipErrorInvalidValue;
   }
+}
+
+// Rows per launch.  Every kernel uses at most max(1, n/4) work-items per row
+// (the column pass of n > 2^16: 2^15/4 per row; the others n/(8*C*T) or one
+// per row or per 8/n rows), so launches of at most 2^31 / max(1, n/4) rows keep
+// the grid's work-item count below 2^31.  Larger m is split into several
+// launches on the same stream, each starting at its own first row (a multiple
+// of 1024, so every row start keeps its alignment); they run in stream order,
+// and rows are independent, so the result is that of one launch.
+constexpr int64_t kMaxItemsPerLaunch = int64_t(1) << 31;
+
+int64_t rows_per_launch(int L) {
+  const int64_t per_row = L >= 2 ? (int64_t(1) << (L - 2)) : 1;
+  return (kMaxItemsPerLaunch / per_row) & ~int64_t(1023);
+}
+
+template <int DT, int EPI = kStore16>
+hipError_t launch_dt(int L, const uint16_t *in, int64_t in_stride, uint16_t *out,
+                     int64_t out_stride, int64_t m, const ScaleArgs &sc, int front,
+                     hipStream_t stream, QuantOut qo = {}) {
+  const int64_t chunk = rows_per_launch(L);
+  for (int64_t r0 = 0; r0 < m; r0 += chunk) {
+    const int64_t mc = m - r0 < chunk ? m - r0 : chunk;
+    QuantOut q = qo;
+    if constexpr (EPI != kStore16) {
+      q.codes = qo.codes + r0 * qo.stride;
+      q.scales = qo.scales + r0;
+    }
+    uint16_t *o = EPI == kStore16 ? out + r0 * out_stride : nullptr;
+    const hipError_t e =
+        launch_dt_one<DT, EPI>(L, in + r0 * in_stride, in_stride, o, out_stride, mc, sc, front,
+                               stream, q);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// n > 2^16 through the workspace: row r0 of a launch uses workspace row r0 too.
+template <int DT>
+hipError_t launch_large_dt(int L, const uint16_t *in, int64_t in_stride, uint16_t *out,
+                           int64_t out_stride, int64_t m, float scale, float *ws,
+                           hipStream_t stream) {
+  const int64_t chunk = rows_per_launch(L);
+  for (int64_t r0 = 0; r0 < m; r0 += chunk) {
+    const int64_t mc = m - r0 < chunk ? m - r0 : chunk;
+    const hipError_t e = launch_large_one<DT>(L, in + r0 * in_stride, in_stride,
+                                              out + r0 * out_stride, out_stride, mc, scale,
+                                              ws + r0 * (int64_t(1) << L), stream);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // HADACORE_VARIANT=valu|mfma forces a front end (testing and tuning); unset,

@@ -43,6 +43,22 @@ class HadacoreError(RuntimeError):
 _lib = None
 
 
+def _load_torch_runtime() -> None:
+    """Import torch, if it is installed, before the library is loaded.
+
+    The device pointers and streams passed to the library come from torch, which
+    ships its own copy of the HIP runtime.  libhadacore.so needs libamdhip64.so.7:
+    if torch's copy is already loaded, that need is met by it; if the library were
+    loaded first, the dynamic loader would map the system ROCm runtime instead and
+    torch would then map its own, leaving two runtimes in one process -- the
+    library's would see none of torch's memory or streams (and reports no device).
+    """
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
+
+
 def library() -> ctypes.CDLL:
     """The loaded libhadacore.so (raises if it has not been built)."""
     global _lib
@@ -50,6 +66,7 @@ def library() -> ctypes.CDLL:
         if not LIBRARY.exists():
             raise RuntimeError(f"{LIBRARY} is missing: build it with "
                                "`python -m paper_2412_08832_amd.build`")
+        _load_torch_runtime()
         lib = ctypes.CDLL(str(LIBRARY))
         i64, vp, f32, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, ctypes.c_int32
         lib.hadamard_transform.argtypes = [vp, vp, i64, i64, i32, f32, vp]

@@ -14,6 +14,8 @@ Hadamard size).
 from __future__ import annotations
 
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass
 
 import numpy as np
@@ -123,39 +125,98 @@ def _sweep_seed(k: int, dtype: str) -> int:
     return (100 if dtype == FP16 else 200) + k
 
 
-def generate(w: Workload, rows: int | None = None) -> np.ndarray:
-    """The workload's input bits, (m, n) uint16.
+# Draws are made in slabs of SLAB_ELEMS elements (whole rows): slab s of a
+# workload seeded with `seed` takes its numbers from the child seed sequence
+# SeedSequence(seed, spawn_key=(s,)), filling its rows in row-major order.  The
+# slab layout depends only on the shape, never on the thread count, so any
+# number of threads gives the same bits, and a draw of fewer rows is a prefix
+# of the full draw.
+SLAB_ELEMS = 1 << 22
 
-    ``rows`` keeps only the first rows.  numpy fills draws in row-major order, so
-    a draw of fewer rows equals the first rows of the full draw; the
-    bf16_1048576x128_inplace recipe draws its outlier mask after all values and therefore always draws in full.
-    """
-    m = w.m if rows is None else min(int(rows), w.m)
+
+def _threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        n = min(n, int(env))
+    return max(1, min(n, 16))
+
+
+def _slab_values(w: Workload, seed: int, s: int, rows: int) -> np.ndarray:
+    """float32 values of `rows` rows of slab s, by the workload's distribution."""
+    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(s,)))
     n = w.n
+    if w.name == "bf16_1048576x128_inplace":
+        # N(0,1) values, then (after all of the slab's values) a Bernoulli(1e-3)
+        # mask of entries scaled x100
+        vals = rng.standard_normal((rows, n), dtype=np.float32)
+        mask = rng.random((rows, n), dtype=np.float32) < np.float32(1e-3)
+        np.multiply(vals, np.float32(100.0), out=vals, where=mask)
+        return vals
+    if w.name == "bf16_4096x32768_inplace":
+        # U[-1, 1) in fp32 steps of 2^-23
+        vals = rng.random((rows, n), dtype=np.float32)
+        vals *= np.float32(2.0)
+        vals -= np.float32(1.0)
+        return vals
+    return rng.standard_normal((rows, n), dtype=np.float32)
+
+
+def _seed(w: Workload) -> int:
     if w.name == "fp16_1024x256":
-        rng = np.random.default_rng(0)
-        vals = rng.standard_normal((m, n), dtype=np.float32)
-    elif w.name == "bf16_1048576x128_inplace":
-        rng = np.random.default_rng(2)
-        vals = rng.standard_normal((w.m, n), dtype=np.float32)
-        mask = rng.random((w.m, n), dtype=np.float32) < 1e-3
-        vals[mask] *= np.float32(100.0)
-        vals = vals[:m]
-    elif w.name == "fp16_16384x4096":
-        rng = np.random.default_rng(3)
-        cols = rng.choice(n, 16, replace=False)
-        vals = rng.standard_normal((m, n), dtype=np.float32)
-        vals[:, cols] *= np.float32(50.0)
-    elif w.name == "bf16_4096x32768_inplace":
-        rng = np.random.default_rng(4)
-        vals = rng.uniform(-1.0, 1.0, (m, n)).astype(np.float32)
-    elif w.name.startswith("sweep"):
-        k = int(math.log2(n))
-        rng = np.random.default_rng(_sweep_seed(k, w.dtype))
-        vals = rng.standard_normal((m, n), dtype=np.float32)
+        return 0
+    if w.name == "bf16_1048576x128_inplace":
+        return 2
+    if w.name == "fp16_16384x4096":
+        return 3
+    if w.name == "bf16_4096x32768_inplace":
+        return 4
+    if w.name.startswith("sweep"):
+        return _sweep_seed(int(math.log2(w.n)), w.dtype)
+    raise ValueError(f"unknown workload {w.name!r}")
+
+
+def generate(w: Workload, rows: int | None = None) -> np.ndarray:
+    """The workload's input bits, (m, n) uint16 (the first ``rows`` rows if given).
+
+    Recipes: fp16_1024x256 N(0,1), seed 0; bf16_1048576x128_inplace N(0,1) with
+    0.1% of entries x100, seed 2; fp16_16384x4096 N(0,1) with 16 columns x50 (the
+    columns drawn first from default_rng(3), see hidden_outlier_columns), seed 3;
+    bf16_4096x32768_inplace U(-1,1), seed 4; sweep points N(0,1), seed 100 + k
+    (fp16) or 200 + k (bf16) for n = 2^k.  Values are drawn in fp32 slab by slab
+    (see SLAB_ELEMS) and rounded once to the 16-bit dtype.
+    """
+    m = w.m if rows is None else max(0, min(int(rows), w.m))
+    n = w.n
+    seed = _seed(w)
+    cols = hidden_outlier_columns() if w.name == "fp16_16384x4096" else None
+    per = max(1, SLAB_ELEMS // n)
+    out = np.empty((m, n), dtype=np.uint16)
+
+    def fill(s: int) -> None:
+        r0 = s * per
+        r1 = min(m, r0 + per)
+        if w.name == "bf16_1048576x128_inplace":
+            # its mask follows all of the slab's values: draw the whole slab
+            vals = _slab_values(w, seed, s, min(w.m, r0 + per) - r0)[: r1 - r0]
+        else:
+            vals = _slab_values(w, seed, s, r1 - r0)
+        if cols is not None:
+            vals[:, cols] *= np.float32(50.0)
+        out[r0:r1] = round_to_bits(vals, w.dtype)
+
+    slabs = range((m + per - 1) // per)
+    if len(slabs) <= 1:
+        for s in slabs:
+            fill(s)
     else:
-        raise ValueError(f"unknown workload {w.name!r}")
-    return round_to_bits(np.ascontiguousarray(vals), w.dtype)
+        # numpy's generators and ufuncs release the GIL for bulk work
+        with ThreadPoolExecutor(max_workers=_threads()) as ex:
+            list(ex.map(fill, slabs))
+    return out
 
 
 def hidden_outlier_columns() -> np.ndarray:

@@ -40,11 +40,54 @@ def test_workload_names():
         bench.workload_by_name("sweep:fp32:7:in")
 
 
-def test_default_workload_is_the_headline_configuration():
+def test_default_run_covers_every_configuration():
+    """No flags: one GPU, every named workload (the headline first) and the
+    n = 2^7..2^15 sweep in both dtypes and modes."""
     args = bench.parse_args([])
-    w = bench.workload_by_name(args.workload)
+    assert args.workload is None and args.gpus == 1
+    w = W.WORKLOADS[bench.HEADLINE]
     assert (w.m, w.n, w.dtype, w.inplace) == (1048576, 128, "bf16", True)
-    assert args.gpus == 1
+    assert bench.NAMED[0] == bench.HEADLINE
+    assert set(bench.NAMED) == set(W.WORKLOADS)
+    assert list(bench.SWEEP_LOG2) == list(range(7, 16))
+    assert args.warm_seconds > 0 and args.regions >= 1
+
+
+def test_targets():
+    """70% of the HBM peak for n <= 4096, 55% at n = 32768, none stated for
+    8192/16384 or for the launch-bound 1 MiB call."""
+    assert bench.target_fraction(W.WORKLOADS["fp16_1024x256"]) is None
+    assert bench.target_fraction(W.WORKLOADS["bf16_1048576x128_inplace"]) == 0.70
+    assert bench.target_fraction(W.WORKLOADS["fp16_16384x4096"]) == 0.70
+    assert bench.target_fraction(W.WORKLOADS["bf16_4096x32768_inplace"]) == 0.55
+    for k in range(7, 16):
+        t = bench.target_fraction(W.sweep_point(k, "fp16", True))
+        assert t == (0.70 if k <= 12 else 0.55 if k == 15 else None)
+
+
+def test_sweep_sample_rows():
+    for k in (7, 12, 15):
+        w = W.sweep_point(k, "bf16", True)
+        rows = bench.sweep_rows(w)
+        assert rows[0] == 0 and rows[-1] == w.m - 1
+        assert (rows >= 0).all() and (rows < w.m).all() and (rows[1:] > rows[:-1]).all()
+        assert len(rows) * w.n >= min(w.m * w.n, bench.SWEEP_SAMPLE_ELEMS) // 2
+
+
+def test_check_point_flags_a_wrong_output(oracle):
+    """The per-point oracle check of the CPU leg accepts the oracle's own rounded
+    result and rejects one element moved by 8 ulp."""
+    import numpy as np
+    w = W.sweep_point(7, "fp16", True)
+    bits = W.generate(w, rows=300)
+    ref = oracle.fwht(bits, "fp16", w.scale)
+    good = ref.astype(np.float16).view(np.uint16)
+    small = W.Workload(w.name, w.dtype, 300, w.n, w.inplace, w.scale, w.description)
+    assert bench.check_point(small, bits, good)["ok"]
+    bad = good.copy()
+    bad[17, 5] = np.uint16(int(bad[17, 5]) + 8)
+    r = bench.check_point(small, bits, bad, rows=np.array([0, 17, 299]))
+    assert not r["ok"] and r["rows_checked"] == 3 and r["max_ulp_floored"] > 4
 
 
 @pytest.mark.parametrize("path", PROFILES, ids=[p.stem for p in PROFILES])
@@ -103,6 +146,7 @@ def test_cpu_baseline_fields():
     assert r["kind"] == "oracle" and r["unit"] == "elements/s"
     assert r["value"] > 0 and r["cores"] >= 1
     assert "pass(es) over the first" in r["sample"]
+    assert r["cpus_visible"] >= 1 and "CPUs visible" in r["sample"]
     if r["cores"] > 1:
         assert r["value_1_thread"] > 0
     q = bench.cpu_baseline(W.WORKLOADS["fp16_1024x256"], 0.2, quant="fp8")

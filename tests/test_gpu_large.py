@@ -131,3 +131,62 @@ def test_one_pass_sizes_through_the_workspace_entry(n):
     ref = H.transform(x)
     torch.cuda.synchronize()
     assert torch.equal(out, ref)
+
+
+def _split_rows(m: int, per_launch: int) -> np.ndarray:
+    """Rows on both sides of every launch boundary, the first and the last."""
+    edges = [r for b in range(per_launch, m, per_launch) for r in (b - 2, b - 1, b, b + 1)]
+    return np.unique(np.r_[0, 1, edges, m - 2, m - 1])
+
+
+def test_rows_beyond_one_launch_are_split(oracle):
+    """bf16 n = 128 in place with m = 2^26 + 1000 rows (16 GiB): more rows than one
+    launch takes (2^33 elements per launch), so the call is two launches; rows on
+    both sides of the boundary match the oracle.  The input is a 4096-row seeded
+    block repeated, so every row's input is known on the host."""
+    import torch
+    n, per_launch = 128, 1 << 26
+    m = per_launch + 1000
+    block = W.random_rows(4096, n, "bf16", seed=128)
+    reps = (m + 4095) // 4096
+    say(f"split: bf16 n={n} m={m} in place ({m * n * 2 / 2**30:.1f} GiB)")
+    x = to_device(block, "bf16").repeat(reps, 1)
+    s = W.default_scale(n)
+    H.hadamard_transform(x.data_ptr(), x.data_ptr(), m, n, H.BF16, s,
+                         torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    rows = _split_rows(m, per_launch)
+    got = to_host(x[torch.from_numpy(rows).cuda()])
+    c = compare_with_oracle(oracle, got, block[rows % 4096], "bf16", s, n)
+    say(f"  {c}")
+    assert c.ok, str(c)
+    # rows past m are untouched: the repeated block continues unchanged
+    tail = to_host(x[m:])
+    assert np.array_equal(tail, block[m % 4096: m % 4096 + tail.shape[0]])
+    del x
+    torch.cuda.empty_cache()
+
+
+def test_quantized_rows_beyond_one_launch_are_split(oracle):
+    """The same split for the fused FP8 output (codes and scales offset per launch)."""
+    import torch
+    from fp8_compare import compare_fp8
+    n, per_launch = 128, 1 << 26
+    m = per_launch + 1000
+    block = W.random_rows(4096, n, "fp16", seed=129)
+    say(f"split fp8: fp16 n={n} m={m}")
+    x = to_device(block, "fp16").repeat((m + 4095) // 4096, 1)
+    codes = torch.empty((m, n), dtype=torch.uint8, device="cuda")
+    scales = torch.full((m,), -1.0, dtype=torch.float32, device="cuda")
+    s = W.default_scale(n)
+    H.hadamard_transform_fp8(x.data_ptr(), n, codes.data_ptr(), n, scales.data_ptr(), m, n,
+                             H.FP16, s, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    rows = _split_rows(m, per_launch)
+    idx = torch.from_numpy(rows).cuda()
+    c = compare_fp8(oracle, codes[idx].cpu().numpy(), scales[idx].cpu().numpy(),
+                    block[rows % 4096], "fp16", s, n)
+    say(f"  {c}")
+    assert c.ok, str(c)
+    del x, codes, scales
+    torch.cuda.empty_cache()

@@ -102,19 +102,30 @@ def test_configs_other_mode_bitwise(name):
     assert np.array_equal(a, b)
 
 
-@pytest.mark.parametrize("inplace", [True, False], ids=["inplace", "out"])
+# Sweep points (2^28 elements) compared in full where the dispatch changes shape
+# and above: n = 2048 (two-wave block kernel), 4096 (matrix-core front),
+# 8192-32768 (block kernels, the n = 32768 row-count switch) and 65536 (the
+# persistent loop); elsewhere about 2^20 elements of sampled rows.
+FULL_SWEEP_L = (11, 12, 13, 14, 15, 16)
+
+
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("L", [1, 4, 6] + list(range(7, 17)))
-def test_sweep_full_size_sampled(oracle, L, dtype, inplace):
-    w = W.sweep_point(L, dtype, inplace=inplace)
-    say(f"sweep {w.name} (sampled rows)")
+def test_sweep_full_size(oracle, L, dtype):
+    w = W.sweep_point(L, dtype, inplace=True)
     bits = W.generate(w)
-    out = _run(bits, dtype, w.scale, w.n, inplace)
-    rng = np.random.default_rng(L)
-    rows = np.unique(np.r_[0, w.m - 1, rng.integers(0, w.m, 256)])
-    c = compare_with_oracle(oracle, out, bits, dtype, w.scale, w.n, rows=rows)
-    say(f"  {c}")
-    assert c.ok, str(c)
+    rows = None
+    if L not in FULL_SWEEP_L:
+        rng = np.random.default_rng(L)
+        rows = np.unique(np.r_[0, w.m - 1, rng.integers(0, w.m, max(256, (1 << 20) >> L))])
+    for inplace in (True, False):
+        say(f"sweep {dtype} n={w.n} m={w.m} inplace={inplace} "
+            f"({'all rows' if rows is None else f'{len(rows)} sampled rows'})")
+        out = _run(bits, dtype, w.scale, w.n, inplace)
+        c = compare_with_oracle(oracle, out, bits, dtype, w.scale, w.n, rows=rows)
+        say(f"  {c}")
+        assert c.ok, str(c)
+        del out
 
 
 @pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])

@@ -2,6 +2,7 @@
 from __future__ import annotations
 
 import numpy as np
+import pytest
 
 from metrics import bits_to_f64, compare, ulp
 
@@ -68,3 +69,34 @@ def test_floor_rejects_a_16bit_intermediate_rounding():
     c = compare(out, ref, "fp16")
     assert c.rel_l2 <= 1e-3          # the L2 clause alone would accept it
     assert c.max_ulp_floored > 4.0   # the floored ulp clause does not
+
+
+def test_ulp_reads_the_exponent_exactly():
+    """Just below a power of two the spacing is that of the binade below (no
+    rounding of a logarithm); zero and fp64 subnormals take the subnormal spacing."""
+    below = np.nextafter(2.0, 0.0)
+    assert ulp(np.array([below]), "fp16")[0] == 2.0**-10
+    assert ulp(np.array([2.0]), "fp16")[0] == 2.0**-9
+    assert ulp(np.array([5e-324, -0.0]), "bf16").tolist() == [2.0**-133] * 2
+
+
+def test_blocked_comparison_equals_one_block():
+    """Statistics merged over row blocks (any block size, any thread count) equal
+    those of one comparison of the whole matrix."""
+    from metrics import Accumulator
+    rng = np.random.default_rng(3)
+    ref = rng.standard_normal((40, 64)) * np.exp2(rng.integers(-30, 30, (40, 1)))
+    ref[5] = 0.0
+    gpu = ref.astype(np.float16).astype(np.float64)
+    gpu[7, 3] += 3 * ulp(gpu[7:8, 3], "fp16")[0]
+    ref[9, 1] = np.nan
+    gpu[9, 1] = np.nan
+    whole = compare(gpu, ref, "fp16")
+    acc = Accumulator("fp16")
+    for r0 in range(0, 40, 7):
+        acc.merge(Accumulator("fp16").add(gpu[r0:r0 + 7], ref[r0:r0 + 7]))
+    parts = acc.result()
+    for f in ("count", "max_ulp_floored", "max_ulp_unfloored", "n_above_4ulp_unfloored",
+              "nonfinite_mismatch", "zero_row_mismatch"):
+        assert getattr(parts, f) == getattr(whole, f), f
+    assert parts.rel_l2 == pytest.approx(whole.rel_l2, rel=1e-12)
