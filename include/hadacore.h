@@ -60,7 +60,8 @@
  * Errors: arguments are validated synchronously before anything is enqueued;
  * on error nothing is enqueued and a nonzero status is returned.  No call
  * aborts or throws.  The library keeps no state beyond a per-device cache of
- * the architecture check and the compute-unit count, and is safe to call from
+ * the architecture check, the compute-unit count and the address of the
+ * scratch array of hadamard_transform_ws_noalloc, and is safe to call from
  * several host threads.
  */
 #ifndef HADACORE_H
@@ -72,7 +73,7 @@
 extern "C" {
 #endif
 
-#define HADACORE_VERSION 10101 /* 1.1.1: very large m split over launches */
+#define HADACORE_VERSION 10200 /* 1.2.0: hadamard_transform_ws_noalloc */
 
 typedef int32_t hadacore_dtype;
 #define HADACORE_FP16 0 /* IEEE binary16 */
@@ -90,6 +91,8 @@ typedef int32_t hadacore_status;
 #define HADACORE_ERROR_UNSUPPORTED_DEVICE 8 /* current device is not gfx950 */
 #define HADACORE_ERROR_TOO_LARGE 9          /* m >= 2^31, or m * row stride > 2^40 */
 #define HADACORE_ERROR_WORKSPACE 10         /* workspace NULL or below the required size */
+#define HADACORE_ERROR_SCRATCH 11           /* hadamard_transform_ws_noalloc: needs more than
+                                               HADACORE_NOALLOC_SCRATCH_BYTES of workspace */
 
 /*
  * hadamard_transform -- out = scale * in * H_n for m dense rows of n elements.
@@ -149,6 +152,33 @@ hadacore_status hadamard_transform_ws(const void *in, int64_t in_row_stride, voi
                                       int64_t out_row_stride, int64_t m, int64_t n,
                                       hadacore_dtype dtype, float scale, void *workspace,
                                       int64_t workspace_bytes, void *stream);
+
+/*
+ * hadamard_transform_ws_noalloc -- hadamard_transform_ws for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): the same kernels and results, with
+ * the fp32 workspace taken from a fixed array inside the library instead of
+ * an argument.  The call itself allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine).
+ *   The array is HADACORE_NOALLOC_SCRATCH_BYTES (32 MiB) of device memory per
+ *   GPU, held from the library's first use on that GPU until the process
+ *   ends; for n > 2^16 the call needs hadamard_transform_workspace_size(m, n)
+ *   <= HADACORE_NOALLOC_SCRATCH_BYTES (m * n <= 2^23 elements: e.g. 64 rows of
+ *   2^17, 8 rows of 2^20) and returns HADACORE_ERROR_SCRATCH beyond that,
+ *   enqueuing nothing.  For n <= 2^16 it is hadamard_transform_strided.
+ *   Every call on one GPU uses that GPU's one array: calls that can overlap
+ *   in time on the same GPU (different streams, host threads) race and give
+ *   undefined results; calls in one stream's order are safe.  Nothing in the
+ *   array needs to start at zero (pass 1 writes all of it before pass 2
+ *   reads).  The first call on a device looks up that device's address of the
+ *   array (HADACORE_ERROR_LAUNCH if the runtime cannot give it); run that call
+ *   outside graph capture.
+ * Other arguments, strides, streams and errors as for hadamard_transform_ws.
+ */
+#define HADACORE_NOALLOC_SCRATCH_BYTES (32LL << 20)
+hadacore_status hadamard_transform_ws_noalloc(const void *in, int64_t in_row_stride, void *out,
+                                              int64_t out_row_stride, int64_t m, int64_t n,
+                                              hadacore_dtype dtype, float scale, void *stream);
 
 /*
  * hadamard_transform_fp8 -- the transform fused with per-row quantization to

@@ -65,6 +65,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <mutex>
 
 #include "hadacore.h"
 
@@ -1745,6 +1746,39 @@ hadacore_status validate(const void *in, int64_t in_row_stride, const void *out,
   return HADACORE_SUCCESS;
 }
 
+// Fixed device workspace of hadamard_transform_ws_noalloc: one array per GPU
+// (each device holds its own copy of this module's globals), kScratchBytes
+// long, alive until the process ends.  Host code never uses the symbol's name
+// as an address: on its first call on a device the entry point asks the
+// runtime for that device's address of the array (hipGetSymbolAddress, with
+// the device current) and keeps it here.  The two-pass kernels write every
+// workspace element in pass 1 before pass 2 reads it, so nothing needs
+// clearing between calls; calls that overlap on one GPU share the array and
+// race.
+constexpr int64_t kScratchBytes = HADACORE_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) float scratch[kScratchBytes / sizeof(float)];
+
+std::atomic<float *> g_scratch[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+// This device's address of `scratch`, or nullptr if the runtime cannot give it.
+float *scratch_address() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  float *p = g_scratch[dev].load(std::memory_order_acquire);
+  if (p != nullptr) return p;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  p = g_scratch[dev].load(std::memory_order_relaxed);
+  if (p == nullptr) {
+    void *addr = nullptr;
+    if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || addr == nullptr)
+      return nullptr;
+    p = static_cast<float *>(addr);
+    g_scratch[dev].store(p, std::memory_order_release);
+  }
+  return p;
+}
+
 }  // namespace
 }  // namespace hadacore
 
@@ -1780,11 +1814,16 @@ extern "C" int64_t hadamard_transform_workspace_size(int64_t m, int64_t n) {
   return 4 * m * n;
 }
 
-extern "C" hadacore_status hadamard_transform_ws(const void *in, int64_t in_row_stride, void *out,
-                                                 int64_t out_row_stride, int64_t m, int64_t n,
-                                                 hadacore_dtype dtype, float scale,
-                                                 void *workspace, int64_t workspace_bytes,
-                                                 void *stream) {
+namespace hadacore {
+namespace {
+
+// hadamard_transform_ws after its workspace has been chosen: `workspace` of
+// `workspace_bytes`, or with `fixed` the scratch array (whose size is the
+// limit, reported as HADACORE_ERROR_SCRATCH).
+hadacore_status transform_two_pass(const void *in, int64_t in_row_stride, void *out,
+                                   int64_t out_row_stride, int64_t m, int64_t n,
+                                   hadacore_dtype dtype, float scale, void *workspace,
+                                   int64_t workspace_bytes, bool fixed, void *stream) {
   int L = 0;
   const hadacore_status st =
       validate(in, in_row_stride, out, out_row_stride, m, n, dtype, scale, &L, kMaxLargeL);
@@ -1795,17 +1834,29 @@ extern "C" hadacore_status hadamard_transform_ws(const void *in, int64_t in_row_
   }
   const int64_t need = hadamard_transform_workspace_size(m, n);
   if (need == 0) return HADACORE_ERROR_TOO_LARGE;
-  if (workspace == nullptr || workspace_bytes < need) return HADACORE_ERROR_WORKSPACE;
-  if ((reinterpret_cast<uintptr_t>(workspace) & 15) != 0) return HADACORE_ERROR_MISALIGNED;
+  if (fixed) {
+    if (need > kScratchBytes) return HADACORE_ERROR_SCRATCH;
+  } else {
+    if (workspace == nullptr || workspace_bytes < need) return HADACORE_ERROR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 15) != 0) return HADACORE_ERROR_MISALIGNED;
+  }
   if ((m * (n >> 15)) >= (int64_t(1) << 31)) return HADACORE_ERROR_TOO_LARGE;
-  uintptr_t ilo, ihi, olo, ohi;
-  row_span(in, in_row_stride, m, n, &ilo, &ihi);
-  row_span(out, out_row_stride, m, n, &olo, &ohi);
-  const uintptr_t wlo = reinterpret_cast<uintptr_t>(workspace);
-  const uintptr_t whi = wlo + (uintptr_t)need;
-  if ((wlo < ihi && ilo < whi) || (wlo < ohi && olo < whi)) return HADACORE_ERROR_OVERLAP;
+  auto overlaps = [&](const void *w) {
+    uintptr_t ilo, ihi, olo, ohi;
+    row_span(in, in_row_stride, m, n, &ilo, &ihi);
+    row_span(out, out_row_stride, m, n, &olo, &ohi);
+    const uintptr_t wlo = reinterpret_cast<uintptr_t>(w);
+    const uintptr_t whi = wlo + (uintptr_t)need;
+    return (wlo < ihi && ilo < whi) || (wlo < ohi && olo < whi);
+  };
+  if (!fixed && overlaps(workspace)) return HADACORE_ERROR_OVERLAP;
   const hadacore_status dev = check_device();
   if (dev != HADACORE_SUCCESS) return dev;
+  if (fixed) {
+    workspace = scratch_address();
+    if (workspace == nullptr) return HADACORE_ERROR_LAUNCH;
+    if (overlaps(workspace)) return HADACORE_ERROR_OVERLAP;
+  }
   const uint16_t *src = static_cast<const uint16_t *>(in);
   uint16_t *dst = static_cast<uint16_t *>(out);
   float *ws = static_cast<float *>(workspace);
@@ -1815,6 +1866,27 @@ extern "C" hadacore_status hadamard_transform_ws(const void *in, int64_t in_row_
           ? launch_large_dt<HADACORE_FP16>(L, src, in_row_stride, dst, out_row_stride, m, scale, ws, s)
           : launch_large_dt<HADACORE_BF16>(L, src, in_row_stride, dst, out_row_stride, m, scale, ws, s);
   return err == hipSuccess ? HADACORE_SUCCESS : HADACORE_ERROR_LAUNCH;
+}
+
+}  // namespace
+}  // namespace hadacore
+
+extern "C" hadacore_status hadamard_transform_ws(const void *in, int64_t in_row_stride, void *out,
+                                                 int64_t out_row_stride, int64_t m, int64_t n,
+                                                 hadacore_dtype dtype, float scale,
+                                                 void *workspace, int64_t workspace_bytes,
+                                                 void *stream) {
+  return transform_two_pass(in, in_row_stride, out, out_row_stride, m, n, dtype, scale, workspace,
+                            workspace_bytes, false, stream);
+}
+
+extern "C" hadacore_status hadamard_transform_ws_noalloc(const void *in, int64_t in_row_stride,
+                                                         void *out, int64_t out_row_stride,
+                                                         int64_t m, int64_t n,
+                                                         hadacore_dtype dtype, float scale,
+                                                         void *stream) {
+  return transform_two_pass(in, in_row_stride, out, out_row_stride, m, n, dtype, scale, nullptr, 0,
+                            true, stream);
 }
 
 extern "C" hadacore_status hadamard_transform(const void *in, void *out, int64_t m, int64_t n,
@@ -1927,6 +1999,9 @@ extern "C" const char *hadacore_status_string(hadacore_status status) {
     case HADACORE_ERROR_TOO_LARGE: return "problem too large for one launch";
     case HADACORE_ERROR_WORKSPACE:
       return "workspace missing or smaller than hadamard_transform_workspace_size(m, n)";
+    case HADACORE_ERROR_SCRATCH:
+      return "workspace needed exceeds the fixed scratch array of hadamard_transform_ws_noalloc "
+             "(HADACORE_NOALLOC_SCRATCH_BYTES)";
     default: return "unknown status";
   }
 }

@@ -6,7 +6,7 @@ directory; if it is missing, every call raises (there is no fallback).
 
 The raw entry points take device addresses as integers and keep the C names:
 ``hadamard_transform``, ``hadamard_transform_strided``, ``hadamard_transform_ws``,
-``hadamard_transform_workspace_size``, ``hadamard_transform_fp8``,
+``hadamard_transform_ws_noalloc``, ``hadamard_transform_workspace_size``, ``hadamard_transform_fp8``,
 ``hadamard_transform_int8``, ``hadacore_stream_copy``, ``hadacore_status_string``,
 ``hadacore_version``.  ``transform``, ``transform_fp8`` and ``transform_int8`` are
 convenience wrappers for 2-D torch tensors on a ROCm device.
@@ -25,10 +25,11 @@ SUCCESS = 0
 STATUS_NAMES = {
     0: "SUCCESS", 1: "INVALID_VALUE", 2: "INVALID_SIZE", 3: "INVALID_DTYPE",
     4: "INVALID_STRIDE", 5: "MISALIGNED", 6: "OVERLAP", 7: "LAUNCH",
-    8: "UNSUPPORTED_DEVICE", 9: "TOO_LARGE", 10: "WORKSPACE",
+    8: "UNSUPPORTED_DEVICE", 9: "TOO_LARGE", 10: "WORKSPACE", 11: "SCRATCH",
 }
+NOALLOC_SCRATCH_BYTES = 32 << 20  # HADACORE_NOALLOC_SCRATCH_BYTES
 EXPORTS = ("hadamard_transform", "hadamard_transform_strided", "hadamard_transform_ws",
-           "hadamard_transform_workspace_size", "hadamard_transform_fp8",
+           "hadamard_transform_ws_noalloc", "hadamard_transform_workspace_size", "hadamard_transform_fp8",
            "hadamard_transform_int8", "hadacore_stream_copy", "hadacore_status_string",
            "hadacore_version")
 
@@ -75,6 +76,8 @@ def library() -> ctypes.CDLL:
         lib.hadamard_transform_strided.restype = i32
         lib.hadamard_transform_ws.argtypes = [vp, i64, vp, i64, i64, i64, i32, f32, vp, i64, vp]
         lib.hadamard_transform_ws.restype = i32
+        lib.hadamard_transform_ws_noalloc.argtypes = [vp, i64, vp, i64, i64, i64, i32, f32, vp]
+        lib.hadamard_transform_ws_noalloc.restype = i32
         lib.hadamard_transform_workspace_size.argtypes = [i64, i64]
         lib.hadamard_transform_workspace_size.restype = i64
         lib.hadamard_transform_fp8.argtypes = [vp, i64, vp, i64, vp, i64, i64, i32, f32, vp]
@@ -121,6 +124,16 @@ def hadamard_transform_ws(in_ptr: int, in_row_stride: int, out_ptr: int, out_row
                                          dtype, scale, workspace_ptr, workspace_bytes, stream)
     if check:
         _check(st, "hadamard_transform_ws")
+    return st
+
+
+def hadamard_transform_ws_noalloc(in_ptr: int, in_row_stride: int, out_ptr: int,
+                                  out_row_stride: int, m: int, n: int, dtype: int, scale: float,
+                                  stream: int = 0, check: bool = True) -> int:
+    st = library().hadamard_transform_ws_noalloc(in_ptr, in_row_stride, out_ptr, out_row_stride,
+                                                 m, n, dtype, scale, stream)
+    if check:
+        _check(st, "hadamard_transform_ws_noalloc")
     return st
 
 
