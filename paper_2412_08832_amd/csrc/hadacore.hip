@@ -962,15 +962,17 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   }
 }
 
-// n = 65536, matrix-core front: the block kernel's row as a persistent loop.
-// A row fills half the register file and 128 KiB of LDS, so a CU holds one
-// workgroup and, without a loop, its HBM traffic would pause while the row is
-// transformed.  Here the grid is one workgroup per CU; each takes rows
-// blockIdx.x, + gridDim.x, ... and issues the loads of PRE chunks of its next
-// row right after the front end of the current one, so they are in flight
-// during the in-wave stages, the exchange and the epilogue.  16-bit output
-// prefetches the whole row (16 chunks, 64 VGPRs beside the 128 fp32 values);
-// the FP8/INT8 epilogues need more registers and prefetch 14, and issue the
+// n = 65536 (and 16-bit n = 32768 from 4096 rows), matrix-core front: the
+// block kernel's row as a persistent loop.  At n = 65536 a row fills half the
+// register file and 128 KiB of LDS, so a CU holds one workgroup and, without a
+// loop, its HBM traffic would pause while the row is transformed.  Here the
+// grid is one workgroup per CU; each takes rows blockIdx.x, + gridDim.x, ...
+// and issues the loads of PRE chunks of its next row right after the front end
+// of the current one, so they are in flight during the in-wave stages, the
+// exchange and the epilogue.  16-bit output prefetches the whole row (n =
+// 65536: 16 chunks, 64 VGPRs beside the 128 fp32 values; n = 32768: 8 chunks,
+// 32 VGPRs beside 64, with the exchange in one 128 KiB pass); the FP8/INT8
+// epilogues at n = 65536 need more registers and prefetch 14, and issue the
 // last C - PRE chunks between their first code stores, as those free
 // registers.  They fit because every address is a wave-uniform base plus one
 // per-lane offset.  Same arithmetic as the block kernel, so the results are
@@ -1049,7 +1051,8 @@ template <int DT, int L, int C, int HALVES, bool NT, int EPI>
 __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_loop_kernel(
     const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc,
     QuantOut qo, int64_t m) {
-  constexpr int PRE = EPI == kStore16 ? C : 14;
+  constexpr int PRE = EPI == kStore16 ? C : (C < 14 ? C : 14);
+  static_assert(PRE <= C, "prefetch at most the row's chunks");
   __shared__ float4 lds[(1 << L) / 4 / HALVES];
   __shared__ float wave_max[(1 << L) / (512 * C)];
   const int lane = threadIdx.x & (kWave - 1);
@@ -1437,9 +1440,9 @@ hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int6
 }
 
 // Launch configuration of one (size, epilogue, front end).
-// Row counts from which n = 32768 takes its long-call shape (bf16, fp16).
-constexpr int64_t kLongCallRowsBf16 = 8192;
-constexpr int64_t kLongCallRowsFp16 = 12288;
+// Rows from which 16-bit n = 32768 runs as the persistent loop (one workgroup
+// per CU, next row prefetched into registers, one 128 KiB exchange pass).
+constexpr int64_t kLoopRows32768 = 4096;
 
 struct Cfg {
   int C;       // chunks of 8 elements per lane
@@ -1507,13 +1510,21 @@ hipError_t launch_front(const uint16_t *in, int64_t in_stride, uint16_t *out, in
                         int64_t m, const ScaleArgs &sc, hipStream_t stream, QuantOut qo) {
   constexpr Cfg c = config<L, EPI, FRONT>();
   if constexpr (L == 15 && EPI == kStore16 && FRONT == kMfma) {
-    // n = 32768: from enough rows, 4 waves of 16 chunks per row beat 8 waves
-    // of 8 (bf16 from 8192 rows: +1-3.5%; fp16 from 12288: +0.2-4.4%).  Below,
-    // their longer-lived workgroups weigh more at the start and end of the
-    // call: bf16 -3% at 4096 rows and -8% at 2048, fp16 mixed at 8192.
-    if (m >= (DT == HADACORE_BF16 ? kLongCallRowsBf16 : kLongCallRowsFp16))
-      return launch_cfg<DT, L, 16, 1, 1, 2, FRONT, EPI>(in, in_stride, out, out_stride, m, sc,
-                                                        stream, qo);
+    // n = 32768 with 16-bit output, from 4096 rows: the persistent loop.  With
+    // one workgroup per CU a lane has 256 VGPRs, enough to hold the next row's
+    // 16-bit chunks beside this row's fp32 values, and all 128 KiB of the row's
+    // exchange fit the LDS in one pass.  Measured against the block kernels
+    // (both dtypes, both modes, bit-identical output): +0.5-5% at 4096 rows,
+    // +3-8% at 8192 and 16384; mixed (-1.4 to +2.9%) at 2048, so fewer rows
+    // keep the block kernel.  FP8/INT8 output lost 8-12% in the loop.
+    if (m >= kLoopRows32768) {
+      const int64_t cus = device_cus();
+      const int64_t blocks = m < cus ? m : cus;
+      hipLaunchKernelGGL((fwht_block_loop_kernel<DT, L, 8, 1, true, EPI>), dim3((uint32_t)blocks),
+                         dim3((1 << L) / (8 * 8)), 0, stream, in, in_stride, out, out_stride, sc,
+                         qo, m);
+      return hipGetLastError();
+    }
   }
   return launch_cfg<DT, L, c.C, c.T, c.WPB, c.HALVES, FRONT, EPI>(in, in_stride, out, out_stride,
                                                                   m, sc, stream, qo);

@@ -104,7 +104,7 @@ def test_configs_other_mode_bitwise(name):
 
 # Sweep points (2^28 elements) compared in full where the dispatch changes shape
 # and above: n = 2048 (two-wave block kernel), 4096 (matrix-core front),
-# 8192-32768 (block kernels, the n = 32768 row-count switch) and 65536 (the
+# 8192-32768 (block kernels; n = 32768 at 8192 rows runs the persistent loop) and 65536 (the
 # persistent loop); elsewhere about 2^20 elements of sampled rows.
 FULL_SWEEP_L = (11, 12, 13, 14, 15, 16)
 
@@ -172,11 +172,13 @@ def test_n65536_nonfinite_rows_between_ordinary_rows(oracle, dtype, inplace, var
 
 
 @pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])
-@pytest.mark.parametrize("dtype,m", [("bf16", 8191), ("bf16", 8192), ("fp16", 12287), ("fp16", 12288)])
-def test_n32768_either_side_of_the_long_call_shape(oracle, dtype, m, inplace):
-    """n = 32768 switches to 16 chunks per lane from 8192 rows (bf16) or 12288
-    rows (fp16); both sides of each switch against the oracle on sampled rows
-    (first, last, random)."""
+@pytest.mark.parametrize("dtype,m", [("bf16", 4095), ("bf16", 4096), ("fp16", 4095), ("fp16", 4096),
+                                     ("bf16", 4099)])
+def test_n32768_either_side_of_the_loop_switch(oracle, dtype, m, inplace):
+    """16-bit n = 32768 runs the persistent loop (one workgroup per CU) from 4096
+    rows and the block kernel below; both sides of the switch against the oracle
+    on sampled rows (first, last, random; 4099 rows leave a few workgroups a
+    seventeenth row)."""
     n = 1 << 15
     say(f"{dtype} n=32768 m={m} inplace={inplace}")
     bits = W.random_rows(m, n, dtype, seed=m)
