@@ -100,10 +100,13 @@ def test_profile_summary_is_consistent(path):
     assert "rocprofv3" in text and "bench.py" in text
     assert re.fullmatch(r"[0-9a-f]{64}", f["source_sha256"])
     alg = float(f["algorithmic_bytes_per_launch"])
-    avg = float(f["kernel_avg_ns_last_200_calls"])
-    assert float(f["achieved_gbs_last_200_calls"]) == pytest.approx(alg / avg, rel=2e-3)
+    avg = float(f["kernel_avg_ns_timed_calls"])
+    assert float(f["achieved_gbs_timed_calls"]) == pytest.approx(alg / avg, rel=2e-3)
     if "traffic_bytes_per_launch" in f:
-        assert float(f["traffic_bytes_per_launch"]) / alg == pytest.approx(1.0, abs=0.01)
+        # per-dispatch constants (code and argument fetches of every XCD) are a
+        # visible fraction only of the 1 MiB call
+        tol = 0.01 if alg >= 1 << 26 else 0.03
+        assert float(f["traffic_bytes_per_launch"]) / alg == pytest.approx(1.0, abs=tol)
 
 
 @pytest.mark.parametrize("path", [p for p in PROFILES if "traffic_bytes_per_launch" in
@@ -125,6 +128,31 @@ def test_counter_summary_names_its_command_and_source(path):
     assert re.fullmatch(r"[0-9a-f]{64}", f["source_sha256"])
     shares = [float(v) for k, v in re.findall(r"^([a-z_]+_share):\s*(\S+)$", text, flags=re.M)]
     assert shares and all(0.0 <= x <= 1.0 for x in shares)
+
+
+def test_default_command_summary_agrees_with_the_bench_line():
+    """The trace of the default bench command: the headline kernel's first timed
+    region, averaged from the trace, agrees with the step time the same run
+    printed (HIP events around that region) within 3%."""
+    paths = [p for p in PROFILES if p.stem.endswith("_default_command")]
+    assert len(paths) == 1
+    f = _profile_fields(paths[0])
+    assert "--steps 20 --warmup 5" in paths[0].read_text()
+    trace_ms = float(f["kernel_avg_ns_first_region"]) / 1e6
+    assert trace_ms == pytest.approx(float(f["bench_ms_per_step_same_run"]), rel=0.03)
+
+
+def test_counter_summaries_cover_both_front_ends():
+    text = (bench.PROFILES / "sq_counters_front_ends_bf16.txt").read_text()
+    for L in (7, 11, 12, 13, 15):
+        for front in ("valu", "mfma"):
+            assert f"HADACORE_VARIANT={front}" in text and f"sweep:bf16:{L}:in" in text
+    blocks = re.findall(r"front: (valu|mfma)\nkernel: \S+\ndispatches: \d+\nvalu_insts_per_512_elements: ([\d.]+)", text)
+    assert len(blocks) == 10
+    # the matrix-core front issues fewer VALU instructions at every size
+    for i in range(0, 10, 2):
+        assert blocks[i][0] == "valu" and blocks[i + 1][0] == "mfma"
+        assert float(blocks[i + 1][1]) < float(blocks[i][1])
 
 
 def test_every_summary_is_checked():
