@@ -24,9 +24,10 @@ def _device():
     torch.cuda.synchronize()
 
 
-CASES = [  # (n, m, dtype, in place): wave kernel, block kernel, persistent loop
+CASES = [  # (n, m, dtype, in place): wave kernel, block kernel, persistent loops
     (128, 4099, "bf16", True),
     (32768, 37, "fp16", False),
+    (32768, 4100, "bf16", True),
     (65536, 300, "bf16", False),
 ]
 

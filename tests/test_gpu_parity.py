@@ -191,6 +191,84 @@ def test_n32768_either_side_of_the_loop_switch(oracle, dtype, m, inplace):
     assert c.ok, str(c)
 
 
+def _loop_rows(m: int, cus: int, special) -> np.ndarray:
+    """Rows to compare in an n = 32768 loop test: the special rows, the rows the
+    same workgroups take next (row + CUs, + 2 CUs), the first and last rows, and
+    random ones."""
+    rng = np.random.default_rng(m)
+    picks = [r + k * cus for r in special for k in (0, 1, 2)]
+    return np.unique(np.clip(np.r_[0, 1, m - 2, m - 1, picks, rng.integers(0, m, 96)], 0, m - 1))
+
+
+@pytest.mark.parametrize("inplace", [False, True], ids=["out", "inplace"])
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_n32768_loop_nonfinite_rows_between_ordinary_rows(oracle, dtype, inplace):
+    """NaN, Inf and zero rows in the persistent n = 32768 loop (4096 + 5 rows, so
+    each workgroup takes ~16 rows): nothing carries over to the rows a workgroup
+    takes after them."""
+    import torch
+    n = 1 << 15
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    m = 4096 + 5
+    say(f"n=32768 loop nonfinite rows m={m} {dtype} inplace={inplace}")
+    bits = W.random_rows(m, n, dtype, seed=3277)
+    nan = 0x7E00 if dtype == "fp16" else 0x7FC0
+    inf = 0x7C00 if dtype == "fp16" else 0x7F80
+    special = [0, 1, 2, cus + 1, cus + 3, 2 * cus, m - 1]
+    bits[0, 11] = nan
+    bits[cus + 1, 5] = nan
+    bits[1, 3] = inf
+    bits[2 * cus, 1] = inf | 0x8000
+    bits[2] = 0
+    bits[cus + 3] = 0
+    bits[m - 1, 7] = nan
+    s = W.default_scale(n)
+    out = _run(bits, dtype, s, n, inplace)
+    c = compare_with_oracle(oracle, out, bits, dtype, s, n, rows=_loop_rows(m, cus, special))
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_n32768_loop_strided_rows_keep_gaps(oracle, dtype):
+    """The n = 32768 loop on strided rows (4099 rows, input stride n + 24, output
+    stride n + 40): the gaps keep their canaries in both modes, and the rows
+    match the oracle and each other."""
+    import torch
+    n = 1 << 15
+    m = 4099
+    in_stride, out_stride = n + 24, n + 40
+    say(f"n=32768 loop strided {dtype} m={m}")
+    bits = W.random_rows(m, n, dtype, seed=3299, stride=in_stride, fill_bits=0x7FC1)
+    s = W.default_scale(n)
+    out = _run(bits, dtype, s, n, False, out_stride=out_stride, out_fill=0x5A5A)
+    assert (out[:, n:] == 0x5A5A).all(), "out-of-place write touched the row gap"
+    rows = _loop_rows(m, torch.cuda.get_device_properties(0).multi_processor_count, [3, 4000])
+    c = compare_with_oracle(oracle, out, bits, dtype, s, n, rows=rows)
+    say(f"  {c}")
+    assert c.ok, str(c)
+    out2 = _run(bits, dtype, s, n, True)
+    assert (out2[:, n:] == 0x7FC1).all(), "in-place write touched the row gap"
+    assert np.array_equal(out2[:, :n], out[:, :n])
+
+
+@pytest.mark.parametrize("dtype,scale", [("bf16", 0.0), ("bf16", -1.0), ("bf16", 1e30), ("fp16", 3.0),
+                                         ("fp16", -0.0078125)])
+def test_n32768_loop_unusual_scales(oracle, dtype, scale):
+    """The n = 32768 loop with scales other than 1/sqrt(n) (zero, negative, far
+    from 1): the scale split into the matrix-core operand and the final factor."""
+    import torch
+    n = 1 << 15
+    m = 4096
+    say(f"n=32768 loop scale={scale} {dtype}")
+    bits = W.random_rows(m, n, dtype, seed=3300)   # N(0,1): |y| * 1e30 stays inside bf16's range
+    out = _run(bits, dtype, scale, n, False)
+    rows = _loop_rows(m, torch.cuda.get_device_properties(0).multi_processor_count, [7])
+    c = compare_with_oracle(oracle, out, bits, dtype, scale, n, rows=rows)
+    say(f"  {c}")
+    assert c.ok, str(c)
+
+
 # scales beyond 1/sqrt(n): zero, negative, not a power of two, far from 1 (kept
 # where the outputs stay inside the dtype's range, so that the comparison with
 # the unrounded oracle is meaningful)
