@@ -49,7 +49,7 @@ PROFILES = ROOT / "profiles"
 HEADLINE = "bf16_1048576x128_inplace"
 NAMED = (HEADLINE, "fp16_1024x256", "fp16_16384x4096", "bf16_4096x32768_inplace")
 SWEEP_LOG2 = range(7, 16)
-SWEEP_SAMPLE_ELEMS = 1 << 20   # oracle-checked elements per sweep point (whole rows)
+SWEEP_SAMPLE_ELEMS = 1 << 22   # oracle-checked elements per sweep point (whole rows)
 
 
 def parse_args(argv=None):
