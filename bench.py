@@ -14,8 +14,8 @@ The default run measures every named workload and the size sweep:
     and out of place (36 points; each input serves both modes).
 Each point warms the GPU up for a fixed time, then times `--steps` back-to-back
 calls in `--regions` separately synchronized regions (the headline's first
-region is the reported step time), and also times a device copy of the same
-bytes.  The CPU-baseline leg then runs the fp64 oracle over every row of the
+region is the reported step time), and also times two device copies of the same
+bytes: the library's 16-byte copy kernel and the runtime's hipMemcpyAsync.  The CPU-baseline leg then runs the fp64 oracle over every row of the
 named workloads and over sampled rows of the sweep points, compares it with one
 fresh-copy call of the transform per point, and times the oracle on the
 headline workload on the host cores.
@@ -238,7 +238,14 @@ def time_point(d: Device, w, pristine, args, quant: str | None = None) -> tuple[
     d.warm(copies, 0, 0.02)
     csec = _median([d.region(copies, args.steps) for _ in range(3)]) / args.steps
     copy_gbs = 2 * nbytes / csec / 1e9
-    del dsts, copies, calls, outs, ins
+    # the runtime's device-to-device copy of the same bytes (torch's copy_ between
+    # contiguous same-dtype tensors on one device is a hipMemcpyAsync): the memcpy
+    # bound the paper compares against (App. B)
+    memcpys = [(lambda i=i: dsts[i].copy_(ins[i])) for i in range(nbuf)]
+    d.warm(memcpys, 0, 0.02)
+    msec = _median([d.region(memcpys, args.steps) for _ in range(3)]) / args.steps
+    memcpy_gbs = 2 * nbytes / msec / 1e9
+    del dsts, copies, memcpys, calls, outs, ins
 
     # one call on a fresh copy of the input, for the oracle check
     x = pristine.clone()
@@ -272,6 +279,7 @@ def time_point(d: Device, w, pristine, args, quant: str | None = None) -> tuple[
         "elements_per_s": w.m * w.n / med, "gbs": gbs, "frac_hbm_peak": gbs / HBM_PEAK_GBS,
         "gbs_best_region": alg_bytes / min(per_call) / 1e9,
         "copy_gbs": copy_gbs, "frac_of_copy": gbs / copy_gbs,
+        "memcpy_gbs": memcpy_gbs, "frac_of_memcpy": gbs / memcpy_gbs,
         "alg_bytes_per_call": alg_bytes,
     }
     if not quant:
@@ -424,6 +432,7 @@ def headline_line(args, w, rec, quant=None) -> dict:
             "scale": w.scale, "rotating_buffers": rec["rotating_buffers"],
             "achieved_gbs": gbs, "frac_hbm_peak": gbs / HBM_PEAK_GBS,
             "copy_gbs": rec["copy_gbs"], "frac_of_copy": gbs / rec["copy_gbs"],
+            "memcpy_gbs": rec["memcpy_gbs"], "frac_of_memcpy": gbs / rec["memcpy_gbs"],
             "timing": f"value and ms_per_step from the first timed region ({args.steps} calls after "
                       f">= {args.warmup} calls and >= {args.warm_seconds} s of warm-up); "
                       f"points report the median of {args.regions} regions",
