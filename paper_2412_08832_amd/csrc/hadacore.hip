@@ -811,44 +811,66 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
 
 // Exchange of the NW wave bits with the low log2(NW) chunk bits through LDS
 // (fp32, in HALVES passes over the 4-element halves of each chunk), then the
-// register stages on the exchanged bits.  LDS word address of tile element
-// ((W*64 + l)*8 + 4h + q) in pass p = h / (2 / HALVES) is
-// ((W*(2/HALVES) + h % (2/HALVES))*64 + l)*4 + q, so each 16-byte access of a
-// wave is 1 KiB contiguous and free of bank conflicts.  After the call, chunk
-// k of wave w holds tile chunk W = (k % NW)*C + (k / NW)*NW + w.  `lead`
-// puts a barrier before the first pass (the LDS is reused from an earlier row).
-template <int C, int NW, int HALVES, int N>
-__device__ __forceinline__ void exchange_wave_bits(float (&v)[N], float4 *lds, int w, int lane,
-                                                   bool lead) {
+// register stages on the exchanged bits.  After the call, chunk k of wave w
+// holds tile chunk W = (k % NW)*C + (k / NW)*NW + w; the wave that held it
+// before is W / C, as its chunk W % C.
+//
+// LDS slot s (16 bytes per lane, 1 KiB per wave access, so no access has a
+// bank conflict) holds, in pass p = h / (2 / HALVES), the half h % (2 /
+// HALVES) of one chunk at float4 index ((s*(2/HALVES) + h % (2/HALVES))*64 +
+// lane).  Two maps from chunks to slots alternate:
+//   direct:     wave w writes its chunk k to slot w*C + k, and reads its
+//               chunk k from slot (k % NW)*C + (k / NW)*NW + w;
+//   transposed: wave w writes its chunk k to slot (k % NW)*C + (k / NW)*NW + w,
+//               and reads its chunk k from slot w*C + k.
+// In both, the writer of a slot is the wave that holds the chunk and the reader
+// the wave that takes it.  Each pass takes the other map from the pass before
+// it (pass 0 the map TR0, pass 1 the other), so the slots a wave writes are
+// exactly those it read itself in the previous pass: a wave can start writing
+// as soon as its own reads of that pass are issued (LDS accesses of one wave
+// run in order), and the only barrier is the one between the writes and the
+// reads of a pass.  A caller that runs several exchanges on the same LDS (the
+// row loops) alternates TR0 accordingly.
+template <int C, int NW, int HALVES, bool TR0, int N>
+__device__ __forceinline__ void exchange_wave_bits(float (&v)[N], float4 *lds) {
   static_assert(NW >= 2 && NW <= C && NW <= 8, "wave bits must fit the chunk bits");
   static_assert(HALVES == 1 || HALVES == 2, "one or two exchange passes");
   constexpr int kParts = 2 / HALVES;
+  // per-lane bases built from threadIdx.x (= w*64 + lane) plus immediate
+  // offsets, rather than a register per distinct uniform part:
+  //   own  = ((w*C)*kParts)*64 + lane, slot w*C + k at + (k*kParts)*64
+  //   gath = (w*kParts)*64 + lane,     slot Wk + w at + (Wk*kParts)*64
+  const int t = (int)threadIdx.x, tw = t & ~(kWave - 1);
+  float4 *own = lds + (t + (C * kParts - 1) * tw);
+  float4 *gath = lds + (t + (kParts - 1) * tw);
 #pragma unroll
   for (int pass = 0; pass < HALVES; ++pass) {
-    if (pass > 0 || lead) __syncthreads();  // earlier reads of the LDS are done
-#pragma unroll
-    for (int k = 0; k < C; ++k) {
-      const int W = w * C + k;
-#pragma unroll
-      for (int hh = 0; hh < kParts; ++hh) {
-        const int h = pass * kParts + hh;
-        lds[(W * kParts + hh) * kWave + lane] =
-            make_float4(v[k * 8 + 4 * h], v[k * 8 + 4 * h + 1], v[k * 8 + 4 * h + 2],
-                        v[k * 8 + 4 * h + 3]);
-      }
-    }
-    __syncthreads();
-    // read slot (W*kParts + hh)*64 + lane with W = Wk + w: one per-lane base
-    // (w*kParts*64 + lane, from threadIdx.x) plus immediate offsets, rather
-    // than a register per distinct uniform part
-    const float4 *rd = lds + (int)(threadIdx.x + (kParts - 1) * (threadIdx.x & ~(kWave - 1)));
+    const bool tr = TR0 != (pass == 1);
+    // keep the passes apart in the schedule (the barrier between them used to):
+    // mixing them keeps more values live and spills at n = 65536
+    if (pass > 0) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const int Wk = (k % NW) * C + (k / NW) * NW;
 #pragma unroll
       for (int hh = 0; hh < kParts; ++hh) {
         const int h = pass * kParts + hh;
-        const float4 f = rd[(Wk * kParts + hh) * kWave];
+        const float4 f = make_float4(v[k * 8 + 4 * h], v[k * 8 + 4 * h + 1],
+                                     v[k * 8 + 4 * h + 2], v[k * 8 + 4 * h + 3]);
+        if (tr)
+          gath[(Wk * kParts + hh) * kWave] = f;
+        else
+          own[(k * kParts + hh) * kWave] = f;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+      const int Wk = (k % NW) * C + (k / NW) * NW;
+#pragma unroll
+      for (int hh = 0; hh < kParts; ++hh) {
+        const int h = pass * kParts + hh;
+        const float4 f = tr ? own[(k * kParts + hh) * kWave] : gath[(Wk * kParts + hh) * kWave];
         v[k * 8 + 4 * h] = f.x;
         v[k * 8 + 4 * h + 1] = f.y;
         v[k * 8 + 4 * h + 2] = f.z;
@@ -865,8 +887,8 @@ __device__ __forceinline__ void exchange_wave_bits(float (&v)[N], float4 *lds, i
 // in-wave stages the wave bits are exchanged with the low log2(NW) chunk bits
 // through LDS (fp32), then finished as register stages.  HALVES = 2 runs the
 // exchange in two passes over the two 4-element halves of each chunk, which
-// halves the LDS footprint (more workgroups per CU) at the cost of two extra
-// barriers.  The exchange keeps every value in its lane, so the lane layout
+// halves the LDS footprint (more workgroups per CU) at the cost of one more
+// barrier.  The exchange keeps every value in its lane, so the lane layout
 // of the front end carries through to the store.  At n = 65536 (C = 16,
 // NW = 8) a lane holds 128 fp32 values, so the 512 lanes of the workgroup
 // keep the whole row in registers (256 KiB, half the CU's register file) and
@@ -929,7 +951,7 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
     if constexpr (kRaise) __builtin_amdgcn_s_setprio(0);
   }
   wave_stages<FRONT, L, C>(v, lane);
-  exchange_wave_bits<C, NW, HALVES>(v, lds, w, lane, false);
+  exchange_wave_bits<C, NW, HALVES, false>(v, lds);
   const int lf = lane_field<FRONT, L>(lane);
   if constexpr (EPI == kStore16) {
     const Finisher<DT, FRONT> fin(twisted<FRONT, L>(lane), sc.post);
@@ -980,7 +1002,7 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
 
 // One row of the loop: transform `raw` (row `row`), prefetch row `row` +
 // gridDim.x into `raw` when it exists, store; returns whether it did.
-template <int DT, int L, int C, int HALVES, bool NT, int EPI, int PRE>
+template <int DT, int L, int C, int HALVES, bool NT, int EPI, int PRE, bool TR0>
 __device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16_t *in,
                                          int64_t in_stride, uint16_t *out, int64_t out_stride,
                                          const ScaleArgs &sc, const QuantOut &qo, int64_t m,
@@ -1009,7 +1031,7 @@ __device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16
     for (int k = 0; k < PRE; ++k) raw[k] = gload_at<NT>(src + (w * C + k) * 512, ld_off);
   }
   wave_stages<kMfma, L, C>(v, lane);
-  exchange_wave_bits<C, NW, HALVES>(v, lds, w, lane, true);
+  exchange_wave_bits<C, NW, HALVES, TR0>(v, lds);
   const int lf = lane_field<kMfma, L>(lane);
   if constexpr (EPI == kStore16) {
     const Finisher<DT, kMfma> fin(twisted<kMfma, L>(lane), sc.post);
@@ -1067,13 +1089,33 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_loop_kernel(
   // re-entered, with the next row's loads older than this row's stores: the
   // compiler's wait before the front end then covers the loads only, not the
   // stores that follow them.
-  if (!loop_row<DT, L, C, HALVES, NT, EPI, PRE>(raw, row, in, in_stride, out, out_stride, sc, qo,
-                                                  m, lds, wave_max, w, lane))
+  //
+  // With two exchange passes every row takes both slot maps; with one,
+  // consecutive rows take them in turn (the loop is unrolled by two).  Either
+  // way the LDS needs no barrier before a row's exchange writes.
+  if (!loop_row<DT, L, C, HALVES, NT, EPI, PRE, false>(raw, row, in, in_stride, out, out_stride,
+                                                         sc, qo, m, lds, wave_max, w, lane))
     return;
-  do {
-    row += gridDim.x;
-  } while (loop_row<DT, L, C, HALVES, NT, EPI, PRE>(raw, row, in, in_stride, out, out_stride, sc,
-                                                      qo, m, lds, wave_max, w, lane));
+  if constexpr (HALVES == 2) {
+    do {
+      row += gridDim.x;
+    } while (loop_row<DT, L, C, HALVES, NT, EPI, PRE, false>(raw, row, in, in_stride, out,
+                                                               out_stride, sc, qo, m, lds,
+                                                               wave_max, w, lane));
+  } else {
+    for (;;) {
+      row += gridDim.x;
+      if (!loop_row<DT, L, C, HALVES, NT, EPI, PRE, true>(raw, row, in, in_stride, out,
+                                                            out_stride, sc, qo, m, lds, wave_max,
+                                                            w, lane))
+        return;
+      row += gridDim.x;
+      if (!loop_row<DT, L, C, HALVES, NT, EPI, PRE, false>(raw, row, in, in_stride, out,
+                                                             out_stride, sc, qo, m, lds, wave_max,
+                                                             w, lane))
+        return;
+    }
+  }
 }
 
 // n <= 8: one row per thread.  A row is n consecutive 16-bit values, 2n bytes
