@@ -118,6 +118,37 @@ __device__ __forceinline__ void gstore_at(void *base, uint32_t off, u4 v) {
   gstore<NT>(reinterpret_cast<uint16_t *>(static_cast<char *>(base) + off), v);
 }
 
+// Output stores from a wave-uniform base.  With SC1, a nontemporal store also
+// sets the SC1 cache-policy bit, which plain C++ cannot ask for, so it goes
+// out as a raw buffer store (a buffer resource over the 4 GiB from the base,
+// so no range check applies) with the policy NT | SC1.  Measured on MI355X
+// against plain nontemporal stores (interleaved, same box, bit-identical
+// outputs): +1.6% to +3.2% for the one-wave-per-row kernels and the dense
+// n <= 4 kernel, +1% to +1.7% in place at n = 4096 and 8192, 0 to +1% for the
+// quantized outputs, the same for the device copy; but -0.2% to -4% for 16-bit
+// rows of 16384 elements and more, which keep plain nontemporal stores.  The
+// cache bits of the loads made no difference.  `base` must be the same in every
+// lane of the wave: it is read from the first active lane.
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer resource word 3 on gfx9: 32-bit data format
+constexpr int kPolicyNtSc1 = 2 | 16;    // buffer cache-policy operand: NT (bit 1) | SC1 (bit 4)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(void *base) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void *>((hi << 32) | lo), (short)0,
+                                           -1, kRsrcWord3);
+}
+
+template <bool NT, bool SC1>
+__device__ __forceinline__ void gstore_u(void *base, uint32_t off, u4 v) {
+  if constexpr (NT && SC1) {
+    __builtin_amdgcn_raw_buffer_store_b128(v, uniform_rsrc(base), (int)off, 0, kPolicyNtSc1);
+  } else {
+    gstore_at<NT>(base, off, v);
+  }
+}
+
 // ---- 16-bit <-> fp32 ------------------------------------------------------
 
 // Widens the packed pair in `u` (element 2i in the low half), multiplies by
@@ -617,6 +648,16 @@ __device__ __forceinline__ void gstore8_at(void *base, uint32_t off, u2 v) {
   }
 }
 
+// 8-byte output store from a wave-uniform base (see gstore_u).
+template <bool NT, bool SC1>
+__device__ __forceinline__ void gstore8_u(void *base, uint32_t off, u2 v) {
+  if constexpr (NT && SC1) {
+    __builtin_amdgcn_raw_buffer_store_b64(v, uniform_rsrc(base), (int)off, 0, kPolicyNtSc1);
+  } else {
+    gstore8_at<NT>(base, off, v);
+  }
+}
+
 // Row scale and quantization multiplier of a lane, given the largest |register|
 // of its row.  The multiplier includes the twist sign (and, for kMfma, the part
 // of the scale the front end left out).  Both correctly rounded quotients come
@@ -688,7 +729,7 @@ struct RowQuant {
 // the last tile can end past row m; it masks those rows.  Addresses are a
 // wave-uniform tile base plus per-lane byte offsets inside the tile, which the
 // row stride limit (2^26 elements) keeps below 2^32.
-template <int DT, int L, int C, int T, int WPB, bool NT, int FRONT, int EPI>
+template <int DT, int L, int C, int T, int WPB, bool NT, int FRONT, int EPI, bool SC1 = false>
 __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
     const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride, int64_t m,
     ScaleArgs sc, QuantOut qo) {
@@ -765,7 +806,7 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
     if constexpr (EPI == kStore16) {
 #pragma unroll
       for (int k = 0; k < C; ++k) {
-        if (kRows == 1 || st_row[k] < cur_valid) gstore_at<NT>(dst, st_off[k], fin(&v[k * 8]));
+        if (kRows == 1 || st_row[k] < cur_valid) gstore_u<NT, SC1>(dst, st_off[k], fin(&v[k * 8]));
       }
     } else {
       // row maxima: within each chunk, across the chunks of one row (chunk
@@ -794,7 +835,7 @@ __global__ __launch_bounds__(kWave *WPB) void fwht_wave_kernel(
         for (int j = 0; j < C; ++j) {
           if ((j & ~kChunkRow) != k) continue;
           if (kRows == 1 || st_row[j] < cur_valid) {
-            gstore8_at<NT>(dst, st_off[j], qz.codes(&v[j * 8]));
+            gstore8_u<NT, SC1>(dst, st_off[j], qz.codes(&v[j * 8]));
           }
         }
         if ((lane & row_lane_mask<FRONT, L>()) == 0 && (kRows == 1 || st_row[k] < cur_valid)) {
@@ -896,7 +937,8 @@ __device__ __forceinline__ void exchange_wave_bits(float (&v)[N], float4 *lds) {
 //
 // IN32 (second pass of n > 2^16): the input rows are fp32, already scaled, and
 // row r of the input is block r & (2^sub - 1) of output row r >> sub.
-template <int DT, int L, int C, int HALVES, bool NT, int FRONT, int EPI, bool IN32 = false>
+template <int DT, int L, int C, int HALVES, bool NT, int FRONT, int EPI, bool IN32 = false,
+          bool SC1 = false>
 __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
     const void *in, int64_t in_stride, uint16_t *out, int64_t out_stride, ScaleArgs sc,
     QuantOut qo, int sub) {
@@ -917,6 +959,8 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
   // was neutral or slower.
   constexpr bool kRaise = !IN32 && !(EPI == kStore16 && DT == HADACORE_FP16);
   if constexpr (kRaise) __builtin_amdgcn_s_setprio(3);
+  // output stores with the SC1 bit (see gstore_u) if asked, except 16-bit rows of 2^14 and more
+  constexpr bool kSc1 = SC1 && (EPI != kStore16 || L <= 13);
 
   float v[C * 8];
   if constexpr (IN32) {
@@ -959,7 +1003,7 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const int W = (k % NW) * C + (k / NW) * NW + w;
-      gstore_at<NT>(dst, (uint32_t)((W * kWave + lf) * 16), fin(&v[k * 8]));
+      gstore_u<NT, kSc1>(dst, (uint32_t)((W * kWave + lf) * 16), fin(&v[k * 8]));
     }
   } else {
     // the row spans the workgroup: registers, then lanes, then waves (through LDS)
@@ -978,7 +1022,7 @@ __global__ __launch_bounds__((1 << L) / (8 * C)) void fwht_block_kernel(
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const int W = (k % NW) * C + (k / NW) * NW + w;
-      gstore8_at<NT>(codes, (uint32_t)((W * kWave + lf) * 8), qz.codes(&v[k * 8]));
+      gstore8_u<NT, kSc1>(codes, (uint32_t)((W * kWave + lf) * 8), qz.codes(&v[k * 8]));
     }
     if (threadIdx.x == 0) qo.scales[row] = qz.scale;
   }
@@ -1039,7 +1083,7 @@ __device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const int W = (k % NW) * C + (k / NW) * NW + w;
-      gstore_at<NT>(dst + W * 512, (uint32_t)(lf * 16), fin(&v[k * 8]));
+      gstore_u<NT, false>(dst + W * 512, (uint32_t)(lf * 16), fin(&v[k * 8]));
     }
   } else {
     // row amax: registers, lanes, then waves through LDS (the exchange's
@@ -1060,7 +1104,7 @@ __device__ __forceinline__ bool loop_row(u4 (&raw)[C], int64_t row, const uint16
 #pragma unroll
     for (int k = 0; k < C; ++k) {
       const int W = (k % NW) * C + (k / NW) * NW + w;
-      gstore8_at<NT>(codes + W * 512, (uint32_t)(lf * 8), qz.codes(&v[k * 8]));
+      gstore8_u<NT, false>(codes + W * 512, (uint32_t)(lf * 8), qz.codes(&v[k * 8]));
       // the chunks not prefetched yet go out as stored chunks free registers
       if (k < C - PRE) raw[PRE + k] = gload_at<NT>(src + (w * C + PRE + k) * 512, ld_off);
     }
@@ -1305,7 +1349,7 @@ __global__ __launch_bounds__(256) void fwht_column_kernel(const uint16_t *in, in
 // is read and written element by element.  Quantized outputs (codes dense as
 // well) store the 8 codes as one 8-byte access and one scale per row; each row
 // has its own amax and both correctly rounded quotients, as in the row kernel.
-template <int DT, int L, bool NT, int EPI>
+template <int DT, int L, bool NT, int EPI, bool SC1 = false>
 __global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uint16_t *out,
                                                          int64_t total, ScaleArgs sc,
                                                          QuantOut qo) {
@@ -1339,7 +1383,8 @@ __global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uin
 #pragma unroll
     for (int q = 0; q < 4; ++q) r[q] = narrow<DT>(v[2 * q], v[2 * q + 1], 0u);
     if (count == 8) {
-      gstore<NT>(out + base, r);
+      // the workgroup's 4 KiB start at a uniform base; this thread's 16 bytes follow
+      gstore_u<NT, SC1>(out + (int64_t)blockIdx.x * 256 * 8, threadIdx.x * 16u, r);
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -1386,12 +1431,21 @@ __global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uin
     // aligned for them; a scales array that is only 4-byte aligned takes the loop
     constexpr uintptr_t kAlign = N <= 2 ? 15 : 7;
     if (count == 8 && N <= 4 && (reinterpret_cast<uintptr_t>(qo.scales) & kAlign) == 0) {
-      if constexpr (N <= 2) {
+      // the workgroup's scales start at a uniform base (see gstore_u)
+      float *sbase = qo.scales + (int64_t)blockIdx.x * 256 * (8 / N);
+      const uint32_t soff = threadIdx.x * (uint32_t)(8 / N) * 4u;
+      if constexpr (N == 1) {
+        // two 16-byte stores 32 bytes apart per lane: each instruction leaves
+        // gaps that the other fills, so these stay ordinary stores, which the
+        // L2 merges into whole lines (with NT | SC1 they ran 3.3x slower)
 #pragma unroll
-        for (int q = 0; q < 8 / N; q += 4)
+        for (int q = 0; q < 8; q += 4)
           *reinterpret_cast<f4 *>(qo.scales + i0 + q) = f4{sc8[q], sc8[q + 1], sc8[q + 2], sc8[q + 3]};
+      } else if constexpr (N == 2) {
+        gstore_u<NT, SC1>(sbase, soff,
+                          __builtin_bit_cast(u4, f4{sc8[0], sc8[1], sc8[2], sc8[3]}));
       } else {
-        *reinterpret_cast<f2 *>(qo.scales + i0) = f2{sc8[0], sc8[1]};
+        gstore8_u<NT, SC1>(sbase, soff, __builtin_bit_cast(u2, f2{sc8[0], sc8[1]}));
       }
     } else {
 #pragma unroll
@@ -1401,7 +1455,7 @@ __global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uin
     const u2 raw = EPI == kFp8 ? to_e4m3x8(w, 1.0f) : to_int8x8(w, 1.0f, 0xFFFFFFFFu);
     const u2 c = EPI == kFp8 ? raw : u2{raw.x & keep[0], raw.y & keep[1]};
     if (count == 8) {
-      gstore8_at<NT>(qo.codes + base, 0u, c);
+      gstore8_u<NT, SC1>(qo.codes + (int64_t)blockIdx.x * 256 * 8, threadIdx.x * 8u, c);
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -1412,11 +1466,12 @@ __global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uin
 }
 
 // 16-byte streaming copy, one access per thread, the bandwidth reference for
-// the transform.
+// the transform (same load and store cache policies as the transform's).
+template <bool SC1>
 __global__ __launch_bounds__(256) void stream_copy_kernel(const uint16_t *src, uint16_t *dst,
                                                           int64_t count) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < count) gstore<true>(dst + i * 8, gload<true>(src + i * 8));
+  const int64_t i0 = (int64_t)blockIdx.x * blockDim.x, i = i0 + threadIdx.x;
+  if (i < count) gstore_u<true, SC1>(dst + i0 * 8, threadIdx.x * 16u, gload<true>(src + i * 8));
 }
 
 // ---- host dispatch ------------------------------------------------------------
@@ -1440,18 +1495,34 @@ ScaleArgs split_scale(float scale, int dtype) {
 
 int device_cus();
 
+// Whether rows of `row_bytes` at `pitch_bytes` from `p` lie in whole 128-byte
+// lines: p is aligned to 128 and either the rows are contiguous or both the
+// row and the pitch are multiples of 128 bytes.  Row bytes 0 checks p only.
+bool whole_lines(const void *p, int64_t pitch_bytes, int64_t row_bytes) {
+  if ((reinterpret_cast<uintptr_t>(p) & 127) != 0) return false;
+  return pitch_bytes == row_bytes || (pitch_bytes % 128 == 0 && row_bytes % 128 == 0);
+}
+
 // C: chunks per lane; T: tiles per wave (wave kernel) ; WPB: waves per workgroup
 // (wave kernel); HALVES: LDS exchange passes (block kernel); FRONT: kValu / kMfma.
 template <int DT, int L, int C, int T, int WPB, int HALVES, int FRONT, int EPI = kStore16>
 hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int64_t out_stride,
                       int64_t m, const ScaleArgs &sc, hipStream_t stream, QuantOut qo = {}) {
+  // output stores with the SC1 bit (see gstore_u) only where every store
+  // instruction writes whole 128-byte lines
+  const bool sc1 = EPI == kStore16 ? whole_lines(out, out_stride * 2, 2 << L)
+                                   : whole_lines(qo.codes, qo.stride, 1 << L);
   if constexpr (L <= 2) {
     const int64_t out_pitch = EPI == kStore16 ? out_stride : qo.stride;
     if (in_stride == (1 << L) && out_pitch == (1 << L)) {
       const int64_t total = m << L;
-      hipLaunchKernelGGL((fwht_dense_kernel<DT, L, true, EPI>),
-                         dim3((uint32_t)((total + 8 * 256 - 1) / (8 * 256))), dim3(256), 0, stream,
-                         in, out, total, sc, qo);
+      const dim3 grid((uint32_t)((total + 8 * 256 - 1) / (8 * 256)));
+      if (sc1 && (EPI == kStore16 || whole_lines(qo.scales, 0, 0)))
+        hipLaunchKernelGGL((fwht_dense_kernel<DT, L, true, EPI, true>), grid, dim3(256), 0, stream,
+                           in, out, total, sc, qo);
+      else
+        hipLaunchKernelGGL((fwht_dense_kernel<DT, L, true, EPI, false>), grid, dim3(256), 0,
+                           stream, in, out, total, sc, qo);
     } else {
       hipLaunchKernelGGL((fwht_row_kernel<DT, L, true, EPI>), dim3((uint32_t)((m + 255) / 256)),
                          dim3(256), 0, stream, in, in_stride, out, out_stride, m, sc, qo);
@@ -1462,10 +1533,13 @@ hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int6
   } else if constexpr ((1 << L) <= 512 * C) {
     constexpr int64_t rows_per_wave = (int64_t)T * ((512 * C) >> L);
     const int64_t waves = (m + rows_per_wave - 1) / rows_per_wave;
-    const int64_t blocks = (waves + WPB - 1) / WPB;
-    hipLaunchKernelGGL((fwht_wave_kernel<DT, L, C, T, WPB, true, FRONT, EPI>),
-                       dim3((uint32_t)blocks), dim3(kWave * WPB), 0, stream, in, in_stride, out,
-                       out_stride, m, sc, qo);
+    const dim3 grid((uint32_t)((waves + WPB - 1) / WPB));
+    if (sc1)
+      hipLaunchKernelGGL((fwht_wave_kernel<DT, L, C, T, WPB, true, FRONT, EPI, true>), grid,
+                         dim3(kWave * WPB), 0, stream, in, in_stride, out, out_stride, m, sc, qo);
+    else
+      hipLaunchKernelGGL((fwht_wave_kernel<DT, L, C, T, WPB, true, FRONT, EPI, false>), grid,
+                         dim3(kWave * WPB), 0, stream, in, in_stride, out, out_stride, m, sc, qo);
   } else if constexpr (L == 16 && FRONT == kMfma) {
     // one resident workgroup per CU, each looping over rows
     const int64_t cus = device_cus();
@@ -1474,9 +1548,16 @@ hipError_t launch_cfg(const uint16_t *in, int64_t in_stride, uint16_t *out, int6
                        dim3((uint32_t)blocks), dim3((1 << L) / (8 * C)), 0, stream, in, in_stride,
                        out, out_stride, sc, qo, m);
   } else {
-    hipLaunchKernelGGL((fwht_block_kernel<DT, L, C, HALVES, true, FRONT, EPI>), dim3((uint32_t)m),
-                       dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out, out_stride, sc,
-                       qo, 0);
+    // 16-bit rows of 2^14 and more store without SC1 (see gstore_u)
+    constexpr bool kMaySc1 = EPI != kStore16 || L <= 13;
+    if (kMaySc1 && sc1)
+      hipLaunchKernelGGL((fwht_block_kernel<DT, L, C, HALVES, true, FRONT, EPI, false, kMaySc1>),
+                         dim3((uint32_t)m), dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out,
+                         out_stride, sc, qo, 0);
+    else
+      hipLaunchKernelGGL((fwht_block_kernel<DT, L, C, HALVES, true, FRONT, EPI, false, false>),
+                         dim3((uint32_t)m), dim3((1 << L) / (8 * C)), 0, stream, in, in_stride, out,
+                         out_stride, sc, qo, 0);
   }
   return hipGetLastError();
 }
@@ -2031,9 +2112,15 @@ extern "C" hadacore_status hadacore_stream_copy(const void *src, void *dst, int6
   if ((count + 255) / 256 >= (int64_t(1) << 31)) return HADACORE_ERROR_TOO_LARGE;
   const hadacore_status dev = check_device();
   if (dev != HADACORE_SUCCESS) return dev;
-  hipLaunchKernelGGL(stream_copy_kernel, dim3((uint32_t)((count + 255) / 256)), dim3(256), 0,
-                     static_cast<hipStream_t>(stream), static_cast<const uint16_t *>(src),
-                     static_cast<uint16_t *>(dst), count);
+  const dim3 grid((uint32_t)((count + 255) / 256));
+  if (whole_lines(dst, 0, 0))
+    hipLaunchKernelGGL(stream_copy_kernel<true>, grid, dim3(256), 0,
+                       static_cast<hipStream_t>(stream), static_cast<const uint16_t *>(src),
+                       static_cast<uint16_t *>(dst), count);
+  else
+    hipLaunchKernelGGL(stream_copy_kernel<false>, grid, dim3(256), 0,
+                       static_cast<hipStream_t>(stream), static_cast<const uint16_t *>(src),
+                       static_cast<uint16_t *>(dst), count);
   return hipGetLastError() == hipSuccess ? HADACORE_SUCCESS : HADACORE_ERROR_LAUNCH;
 }
 

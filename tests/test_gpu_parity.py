@@ -443,3 +443,75 @@ def test_stream_copy():
                            torch.cuda.current_stream().cuda_stream)
     torch.cuda.synchronize()
     assert torch.equal(src, dst)
+
+
+# Output stores take the SC1 cache bit only where every store writes whole
+# 128-byte lines (output 128-byte aligned, rows contiguous or 128-byte pitched);
+# elsewhere plain nontemporal stores.  The two paths must give the same bytes
+# and write nothing outside the output.
+ALIGN_CASES = [(2, "bf16", 4099), (4, "bf16", 4099), (32, "bf16", 1001), (128, "bf16", 1001),
+               (128, "fp16", 64), (1024, "fp16", 37), (4096, "bf16", 37), (8192, "bf16", 21),
+               (16384, "bf16", 5)]
+
+
+@pytest.mark.parametrize("n,dtype,m", ALIGN_CASES)
+def test_output_alignment_picks_store_path_not_result(oracle, n, dtype, m):
+    import torch
+    s = W.default_scale(n)
+    bits = W.random_rows(m, n, dtype, seed=n + m)
+    x = to_device(bits, dtype)
+    outs = {}
+    for off in (0, 16, 64):  # bytes past a 256-byte aligned allocation
+        pad = 256 // 2
+        buf = torch.full((pad + m * n + pad,), -1, dtype=torch.int16, device="cuda")
+        out = buf[pad + off // 2: pad + off // 2 + m * n]
+        H.hadamard_transform(x.data_ptr(), out.data_ptr(), m, n, CODE[dtype], s,
+                             torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        host = buf.cpu().numpy()
+        lo, hi = pad + off // 2, pad + off // 2 + m * n
+        assert (host[:lo] == -1).all() and (host[hi:] == -1).all(), f"write outside the output (offset {off})"
+        outs[off] = host[lo:hi].copy()
+    assert np.array_equal(outs[0], outs[16]) and np.array_equal(outs[0], outs[64])
+    c = compare_with_oracle(oracle, outs[0].view(np.uint16).reshape(m, n), bits, dtype, s, n)
+    say(f"  n={n} {dtype} m={m}: {c}")
+    assert c.ok, str(c)
+
+
+@pytest.mark.parametrize("n,m", [(1, 4099), (2, 4099), (4, 4099), (128, 1001), (16384, 5)])
+@pytest.mark.parametrize("fmt", ["fp8", "int8"])
+def test_code_and_scale_alignment_picks_store_path_not_result(n, m, fmt):
+    import torch
+    s = W.default_scale(n)
+    bits = W.random_rows(m, n, "bf16", seed=3 * n + m)
+    x = to_device(bits, "bf16")
+    fn = H.hadamard_transform_fp8 if fmt == "fp8" else H.hadamard_transform_int8
+    got = []
+    for coff, soff in ((0, 0), (16, 4), (64, 16)):
+        cbuf = torch.full((256 + m * n + 256,), 0x5A, dtype=torch.uint8, device="cuda")
+        sbuf = torch.full((64 + m + 64,), -7.0, dtype=torch.float32, device="cuda")
+        codes = cbuf[256 + coff: 256 + coff + m * n]
+        scales = sbuf[64 + soff // 4: 64 + soff // 4 + m]
+        fn(x.data_ptr(), n, codes.data_ptr(), n, scales.data_ptr(), m, n, H.BF16, s,
+           torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        ch, sh = cbuf.cpu().numpy(), sbuf.cpu().numpy()
+        c0, s0 = 256 + coff, 64 + soff // 4
+        assert (ch[:c0] == 0x5A).all() and (ch[c0 + m * n:] == 0x5A).all()
+        assert (sh[:s0] == -7.0).all() and (sh[s0 + m:] == -7.0).all()
+        got.append((ch[c0:c0 + m * n].copy(), sh[s0:s0 + m].view(np.uint32).copy()))
+    for c, sc in got[1:]:
+        assert np.array_equal(c, got[0][0]) and np.array_equal(sc, got[0][1])
+
+
+def test_stream_copy_unaligned_destination():
+    import torch
+    src = torch.randint(-30000, 30000, (1 << 20,), dtype=torch.int16, device="cuda")
+    for off in (0, 8, 32):  # 16-bit elements: 0, 16 and 64 bytes
+        buf = torch.full((src.numel() + 256,), 7, dtype=torch.int16, device="cuda")
+        dst = buf[128 + off: 128 + off + src.numel()]
+        H.hadacore_stream_copy(src.data_ptr(), dst.data_ptr(), src.numel() * 2,
+                               torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        assert torch.equal(src, dst)
+        assert (buf[:128 + off] == 7).all() and (buf[128 + off + src.numel():] == 7).all()
