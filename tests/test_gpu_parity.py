@@ -449,7 +449,7 @@ def test_stream_copy():
 # 128-byte lines (output 128-byte aligned, rows contiguous or 128-byte pitched);
 # elsewhere plain nontemporal stores.  The two paths must give the same bytes
 # and write nothing outside the output.
-ALIGN_CASES = [(2, "bf16", 4099), (4, "bf16", 4099), (32, "bf16", 1001), (128, "bf16", 1001),
+ALIGN_CASES = [(2, "bf16", 4099), (4, "bf16", 4099), (8, "fp16", 4099), (32, "bf16", 1001), (128, "bf16", 1001),
                (128, "fp16", 64), (1024, "fp16", 37), (4096, "bf16", 37), (8192, "bf16", 21),
                (16384, "bf16", 5)]
 
@@ -478,7 +478,7 @@ def test_output_alignment_picks_store_path_not_result(oracle, n, dtype, m):
     assert c.ok, str(c)
 
 
-@pytest.mark.parametrize("n,m", [(1, 4099), (2, 4099), (4, 4099), (128, 1001), (16384, 5)])
+@pytest.mark.parametrize("n,m", [(1, 4099), (2, 4099), (4, 4099), (8, 4099), (128, 1001), (16384, 5)])
 @pytest.mark.parametrize("fmt", ["fp8", "int8"])
 def test_code_and_scale_alignment_picks_store_path_not_result(n, m, fmt):
     import torch
