@@ -57,6 +57,11 @@
  * into several launches of consecutive rows on the same stream, with the
  * same result.
  *
+ * Output alignment (performance only): an output (or code array) that starts
+ * on a 128-byte boundary, with contiguous rows or a row pitch and row size
+ * that are multiples of 128 bytes, takes a store path that is 1-3% faster at
+ * most sizes.  Any other valid layout gives the same bytes.
+ *
  * Errors: arguments are validated synchronously before anything is enqueued;
  * on error nothing is enqueued and a nonzero status is returned.  No call
  * aborts or throws.  The library keeps no state beyond a per-device cache of
