@@ -123,11 +123,14 @@ __device__ __forceinline__ void gstore_at(void *base, uint32_t off, u4 v) {
 // out as a raw buffer store (a buffer resource over the 4 GiB from the base,
 // so no range check applies) with the policy NT | SC1.  Measured on MI355X
 // against plain nontemporal stores (interleaved, same box, bit-identical
-// outputs): +1.6% to +3.2% for the one-wave-per-row kernels and the dense
-// n <= 4 kernel, +1% to +1.7% in place at n = 4096 and 8192, 0 to +1% for the
-// quantized outputs, the same for the device copy; but -0.2% to -4% for 16-bit
-// rows of 16384 elements and more, which keep plain nontemporal stores.  The
-// cache bits of the loads made no difference.  `base` must be the same in every
+// outputs): +1.5% to +3.3% for the wave kernel (n <= 512) and the n <= 8
+// kernels, +1% to +2.2% in place at n = 2048-8192, 0 to +2.7% for the
+// quantized outputs, +1.8% for the device copy; but -0.2% to -4% for 16-bit
+// rows of 16384 elements and more, which keep plain nontemporal stores.  A
+// store instruction that leaves part of a 128-byte line unwritten is costly
+// with SC1 (-9% to -18% for unaligned strided rows), so the dispatcher asks
+// for it only where every store writes whole lines (whole_lines).  The cache
+// bits of the loads made no difference.  `base` must be the same in every
 // lane of the wave: it is read from the first active lane.
 constexpr int kRsrcWord3 = 0x00020000;  // raw buffer resource word 3 on gfx9: 32-bit data format
 constexpr int kPolicyNtSc1 = 2 | 16;    // buffer cache-policy operand: NT (bit 1) | SC1 (bit 4)
