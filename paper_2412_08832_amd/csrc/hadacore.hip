@@ -1465,7 +1465,34 @@ __global__ __launch_bounds__(256) void fwht_dense_kernel(const uint16_t *in, uin
       // the workgroup's scales start at a uniform base (see gstore_u)
       float *sbase = qo.scales + (int64_t)blockIdx.x * 256 * (8 / N);
       const uint32_t soff = threadIdx.x * (uint32_t)(8 / N) * 4u;
-      if constexpr (N == 1) {
+      // first row of this wave (its 64 threads hold 512 consecutive rows)
+      const int64_t wave_row = ((int64_t)blockIdx.x * 256 + (threadIdx.x & ~63u)) * 8;
+      if constexpr (N == 1 && SC1) {
+        if (wave_row + 512 <= total) {
+          // A lane holds the scales of 8 consecutive rows; written as they are,
+          // each 16-byte store instruction would leave gaps.  Two lane
+          // shuffles give each instruction a contiguous 1 KiB instead: lane l
+          // stores rows 4l..4l+3 and then 256+4l..256+4l+3 of the wave, held
+          // by lanes l/2 and 32+l/2 (their first or second four, by l's parity).
+          const int lane = threadIdx.x & 63;
+          const bool odd = (lane & 1) != 0;
+          f4 a, b;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float a0 = __shfl(sc8[q], lane >> 1), a1 = __shfl(sc8[4 + q], lane >> 1);
+            const float b0 = __shfl(sc8[q], 32 + (lane >> 1)), b1 = __shfl(sc8[4 + q], 32 + (lane >> 1));
+            a[q] = odd ? a1 : a0;
+            b[q] = odd ? b1 : b0;
+          }
+          float *wbase = qo.scales + wave_row;
+          gstore_u<NT, true>(wbase, (uint32_t)lane * 16u, __builtin_bit_cast(u4, a));
+          gstore_u<NT, true>(wbase + 256, (uint32_t)lane * 16u, __builtin_bit_cast(u4, b));
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; q += 4)
+            *reinterpret_cast<f4 *>(qo.scales + i0 + q) = f4{sc8[q], sc8[q + 1], sc8[q + 2], sc8[q + 3]};
+        }
+      } else if constexpr (N == 1) {
         // two 16-byte stores 32 bytes apart per lane: each instruction leaves
         // gaps that the other fills, so these stay ordinary stores, which the
         // L2 merges into whole lines (with NT | SC1 they ran 3.3x slower)
