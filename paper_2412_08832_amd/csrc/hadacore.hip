@@ -1320,7 +1320,7 @@ __global__ __launch_bounds__(256) void fwht_row_kernel(const uint16_t *in, int64
 // the 8 columns of one lane l of one tile (16-byte load, two 16-byte stores);
 // CW = 4 (A >= 16, to keep A*CW <= 128 values): the 4 columns of one half
 // (8-byte load, one 16-byte store), waves ordered by (tile, half).
-template <int DT, int A, int CW, bool NT>
+template <int DT, int A, int CW, bool NT, bool SC1 = false>
 __global__ __launch_bounds__(256) void fwht_column_kernel(const uint16_t *in, int64_t in_stride,
                                                           float *ws, int64_t m, float scale) {
   static_assert(CW == 8 || CW == 4, "8 or 4 columns per thread");
@@ -1362,13 +1362,16 @@ __global__ __launch_bounds__(256) void fwht_column_kernel(const uint16_t *in, in
     }
   }
   float *dst = ws + i * (int64_t)(A * kBlock) + p;
+  // a wave's 64 threads are lanes l = 0..63 of one (row, tile, half): their
+  // stores start at the wave-uniform dst - 4l (see gstore_u)
+  float *wdst = dst - l * 4;
 #pragma unroll
   for (int t = 0; t < A; ++t) {
-    float *o = dst + (int64_t)t * kBlock;
 #pragma unroll
     for (int hh = 0; hh < CW / 4; ++hh) {
       const f4 x = {v[t][4 * hh], v[t][4 * hh + 1], v[t][4 * hh + 2], v[t][4 * hh + 3]};
-      gstore_at<NT>(o, (uint32_t)(hh * 1024), __builtin_bit_cast(u4, x));
+      gstore_u<NT, SC1>(wdst + (int64_t)t * kBlock, (uint32_t)(l * 16 + hh * 1024),
+                        __builtin_bit_cast(u4, x));
     }
   }
 }
@@ -1766,8 +1769,13 @@ hipError_t launch_large(const uint16_t *in, int64_t in_stride, uint16_t *out, in
   constexpr int CW = A <= 8 ? 8 : 4;
   constexpr int kBlock = 1 << 15;
   const int64_t threads = m * (kBlock / CW);
-  hipLaunchKernelGGL((fwht_column_kernel<DT, A, CW, true>), dim3((uint32_t)((threads + 255) / 256)),
-                     dim3(256), 0, stream, in, in_stride, ws, m, scale);
+  const dim3 grid((uint32_t)((threads + 255) / 256));
+  if (whole_lines(ws, 0, 0))
+    hipLaunchKernelGGL((fwht_column_kernel<DT, A, CW, true, true>), grid, dim3(256), 0, stream, in,
+                       in_stride, ws, m, scale);
+  else
+    hipLaunchKernelGGL((fwht_column_kernel<DT, A, CW, true, false>), grid, dim3(256), 0, stream, in,
+                       in_stride, ws, m, scale);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   constexpr Cfg c = config<15, kStore16, kValu>();

@@ -190,3 +190,29 @@ def test_quantized_rows_beyond_one_launch_are_split(oracle):
     assert c.ok, str(c)
     del x, codes, scales
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("L", [17, 20])
+def test_workspace_alignment_picks_store_path_not_result(L):
+    """The column pass stores to the workspace with the SC1 cache bit only when
+    the workspace is 128-byte aligned; a 16-byte aligned workspace takes plain
+    stores.  Same output bits, and nothing written past the workspace."""
+    import torch
+    n = 1 << L
+    m = 3
+    bits = W.random_rows(m, n, "bf16", seed=L)
+    x = to_device(bits, "bf16")
+    s = W.default_scale(n)
+    need = H.hadamard_transform_workspace_size(m, n)
+    outs = []
+    for off in (0, 16):
+        buf = torch.full((256 + need + 256,), 0x5C, dtype=torch.uint8, device="cuda")
+        ws = buf[256 + off: 256 + off + need]
+        out = torch.empty_like(x)
+        H.hadamard_transform_ws(x.data_ptr(), n, out.data_ptr(), n, m, n, H.BF16, s, ws.data_ptr(),
+                                need, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        host = buf.cpu().numpy()
+        assert (host[:256 + off] == 0x5C).all() and (host[256 + off + need:] == 0x5C).all()
+        outs.append(to_host(out))
+    assert np.array_equal(outs[0], outs[1])
