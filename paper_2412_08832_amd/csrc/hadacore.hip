@@ -1669,8 +1669,7 @@ constexpr Cfg config() {
     if constexpr (L == 15) return {8, 1, 1, 2};
     return {16, 1, 1, 2};  // n = 65536: the row in registers, exchanged in two 128 KiB halves
   } else if constexpr (FRONT == kMfma) {
-    if constexpr (L == 7) return {2, 1, 1, 1};
-    if constexpr (L == 8) return {1, 4, 1, 1};
+    if constexpr (L <= 8) return {2, 1, 1, 1};
     if constexpr (L == 9 || L == 10) return {4, 1, 1, 1};
     if constexpr (L == 11 || L == 12) return {8, 1, 1, 1};
     if constexpr (L <= 15) return {8, 1, 1, 2};
